@@ -1,0 +1,141 @@
+"""Seeded synthetic inputs for the W4Ax path (shared by the tests, the smoke
+check and the benchmark; holds none of the method's arithmetic).
+
+Generator: counter-based.  For tensor ``tid`` of seed ``seed`` the key is
+``mix64(seed * 2**32 + tid)``; element ``i`` draws two 64-bit words
+``mix64(key + (2i+1) * GOLDEN)`` and ``mix64(key + (2i+2) * GOLDEN)``, where
+``mix64`` is the SplitMix64 finaliser (Steele, Lea, Flood, OOPSLA 2014).  The
+top 53 bits of each word give uniforms u1, u2 in [0, 1); the Box-Muller
+transform z = sqrt(-2 ln(1 - u1)) cos(2 pi u2) in fp64 gives a standard normal,
+which is scaled and rounded to fp16 (round to nearest even).  The result
+depends only on (seed, tid, i), not on chunking or thread count.
+
+Workload recipe (synthetic LLaMA-shaped layers):
+  * activations X [M][K] ~ N(0, 1); the channels of every 8-bit block are
+    multiplied by 50 before rounding (outlier channels);
+  * weights W [N][K] ~ N(0, 0.02^2);
+  * block precision map: a contiguous run of 8-bit blocks starting at block
+    floor(3 * NG / 8), or a seeded random subset of blocks.
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+GOLDEN = np.uint64(0x9E3779B97F4A7C15)
+_M1 = np.uint64(0xBF58476D1CE4E5B9)
+_M2 = np.uint64(0x94D049BB133111EB)
+
+TID_X = 1
+TID_W = 2
+TID_MAP = 3
+
+_CHUNK = 1 << 22
+
+
+def mix64(z: np.ndarray) -> np.ndarray:
+    z = z.copy()
+    z ^= z >> np.uint64(30)
+    z *= _M1
+    z ^= z >> np.uint64(27)
+    z *= _M2
+    z ^= z >> np.uint64(31)
+    return z
+
+
+def _key(seed: int, tid: int) -> np.uint64:
+    return mix64(np.array([(seed << 32) + tid], dtype=np.uint64))[0]
+
+
+def _normal_chunk(key: np.uint64, start: int, count: int) -> np.ndarray:
+    i = np.arange(start, start + count, dtype=np.uint64)
+    with np.errstate(over="ignore"):
+        w1 = mix64(key + (np.uint64(2) * i + np.uint64(1)) * GOLDEN)
+        w2 = mix64(key + (np.uint64(2) * i + np.uint64(2)) * GOLDEN)
+    u1 = (w1 >> np.uint64(11)).astype(np.float64) * (1.0 / 9007199254740992.0)
+    u2 = (w2 >> np.uint64(11)).astype(np.float64) * (1.0 / 9007199254740992.0)
+    return np.sqrt(-2.0 * np.log1p(-u1)) * np.cos(2.0 * np.pi * u2)
+
+
+def _threads() -> int:
+    n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def normal_fp16(seed: int, tid: int, shape, std: float = 1.0, col_scale=None) -> np.ndarray:
+    """fp16 bit patterns (uint16) of N(0, std^2) draws; ``col_scale`` (fp64 vector
+    over the last axis) multiplies columns before rounding."""
+    shape = tuple(int(s) for s in shape)
+    total = int(np.prod(shape)) if shape else 1
+    out = np.empty(total, dtype=np.float16)
+    key = _key(seed, tid)
+    ncol = shape[-1] if shape else 1
+    cs = None if col_scale is None else np.asarray(col_scale, dtype=np.float64)
+
+    def work(start):
+        cnt = min(_CHUNK, total - start)
+        z = _normal_chunk(key, start, cnt) * std
+        if cs is not None:
+            z *= cs[(np.arange(start, start + cnt) % ncol)]
+        out[start:start + cnt] = z.astype(np.float16)
+
+    starts = list(range(0, total, _CHUNK))
+    if len(starts) == 1:
+        work(0)
+    else:
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(work, starts))
+    return out.view(np.uint16).reshape(shape)
+
+
+def prec_map(NG: int, n8: int, placement: str = "contiguous", seed: int = 0,
+             start: int | None = None) -> np.ndarray:
+    """uint8 [NG] of 4/8 with ``n8`` 8-bit blocks.
+
+    contiguous: a run starting at ``start`` (default floor(3 NG / 8)), wrapped at NG;
+    random: a seeded subset drawn by a Fisher-Yates shuffle on counter-based words.
+    """
+    m = np.full(NG, 4, dtype=np.uint8)
+    n8 = int(n8)
+    if n8 <= 0:
+        return m
+    if n8 > NG:
+        raise ValueError("more 8-bit blocks than blocks")
+    if placement == "contiguous":
+        s = (3 * NG) // 8 if start is None else int(start)
+        for j in range(n8):
+            m[(s + j) % NG] = 8
+    elif placement == "random":
+        key = _key(seed, TID_MAP)
+        with np.errstate(over="ignore"):
+            words = mix64(key + (np.arange(NG, dtype=np.uint64) + np.uint64(1)) * GOLDEN)
+        idx = list(range(NG))
+        for i in range(NG - 1, 0, -1):
+            j = int(words[i] % np.uint64(i + 1))
+            idx[i], idx[j] = idx[j], idx[i]
+        m[np.array(idx[:n8])] = 8
+    else:
+        raise ValueError(placement)
+    return m
+
+
+def outlier_scale(prec: np.ndarray, G: int = 128, factor: float = 50.0) -> np.ndarray:
+    """Per-channel multiplier: ``factor`` on the channels of 8-bit blocks, else 1."""
+    return np.repeat(np.where(np.asarray(prec) == 8, factor, 1.0), G)
+
+
+def activations(seed: int, M: int, K: int, prec: np.ndarray, G: int = 128) -> np.ndarray:
+    return normal_fp16(seed, TID_X, (M, K), 1.0, outlier_scale(prec, G))
+
+
+def weights(seed: int, N: int, K: int) -> np.ndarray:
+    return normal_fp16(seed, TID_W, (N, K), 0.02)
+
+
+# Layer shapes of the synthetic workloads (tokens M; K -> N).
+LLAMA3_8B = {"qkv": (4096, 6144), "o": (4096, 4096), "gate_up": (4096, 28672),
+             "down": (14336, 4096)}
+LLAMA3_70B = {"qkv": (8192, 10240), "o": (8192, 8192), "gate_up": (8192, 57344),
+              "down": (28672, 8192)}
