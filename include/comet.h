@@ -1,0 +1,145 @@
+/*
+ * comet.h -- C ABI of libcomet, an MI355X (gfx950) implementation of the hot
+ * path of COMET (arXiv 2410.12168): FMPQ activation quantization and the W4Ax
+ * mixed-precision GEMM.
+ *
+ * The method (paper, Sec. 3.2 and Sec. 4):
+ *   - activations are split along the channel dimension only, into blocks of
+ *     G = 128 channels; each block is stored as 4-bit or 8-bit codes with one
+ *     scale per (token, block); weights are 4-bit with one scale per
+ *     (output channel, block);
+ *   - the GEMM contracts the codes block by block with exact integer products,
+ *     dequantizes each block's result by its two scales and sums the blocks
+ *     (Sec. 4.1; the product O = WX of Sec. 5 is out = X W^T here).
+ *
+ * Numbers and encodings (identical, byte for byte, to the CPU oracle):
+ *   - fp16 buffers hold IEEE binary16 bit patterns (uint16_t).
+ *   - Block quantizer: s = fp16_rne(fp32(amax / qmax)), qmax = 7 (4-bit) or
+ *     127 (8-bit); code q = clamp(rint_even(fp32(x / s)), -qmax, qmax);
+ *     s == 0 gives all-zero codes.  Codes -8 / -128 are never produced.
+ *   - A code is stored sign-magnitude.  4-bit chunk (one row, one block,
+ *     G/2 = 64 bytes): for dword j and byte k (0..3) of that dword
+ *         bit 7 = sign of code 8j+k,        bits 6..4 = |code 8j+4+k|,
+ *         bit 3 = sign of code 8j+4+((k+3)%4), bits 2..0 = |code 8j+k|.
+ *     With this layout (dword & 0x87878787) and (rotr(dword, 4) & 0x87878787)
+ *     are the OCP FP8-E4M3 encodings of codes 8j..8j+3 and 8j+4..8j+7 times
+ *     2^-9 (the paper's "location switch" of Sec. 4.3, re-derived so that the
+ *     int4 -> MFMA-operand conversion is two masks and one rotate).
+ *     8-bit chunk (G = 128 bytes): byte c = (sign << 7) | |code c|.
+ *   - A_packed: block-major.  Block g starts at byte M * sum_{g'<g} B(p[g']),
+ *     B(4) = 64, B(8) = 128; row m of block g follows at + m * B(p[g]).
+ *   - a_scales: fp16 [K/G][M];  W_packed: [N][K/2] row-major, row n block g at
+ *     byte n*K/2 + 64*g;  w_scales: fp16 [K/G][N];  out: fp16 [M][N] row-major.
+ *
+ * Conventions for every call:
+ *   - Device pointers are caller-owned HIP device allocations on the current
+ *     device; the library never frees or retains them.  Work is enqueued on
+ *     `stream` (0 = null stream) and returns immediately; the caller keeps the
+ *     buffers alive until the stream has finished.
+ *   - group_prec_map is a HOST array of K/G bytes, each 4 or 8 (the block
+ *     precisions chosen offline by data sampling, Sec. 3.2).  It is read
+ *     during the call and not retained.
+ *   - Every argument is checked before anything is enqueued; on an error
+ *     nothing is launched and comet_last_error() says why.
+ *       COMET_ERR_INVALID_ARG : null pointer, M/N/K < 1, K % G != 0,
+ *                               N % 16 != 0 (GEMM), device pointer not 16-byte
+ *                               aligned, map entry not in {4, 8}, bad window.
+ *       COMET_ERR_UNSUPPORTED : G != 128 (the paper's k = 128), K > 65536,
+ *                               or a current device that is not gfx950.
+ *       COMET_ERR_HIP         : a HIP runtime or launch error.
+ *       COMET_ERR_OOM         : the library could not allocate its workspace.
+ *   - Faults inside kernels surface at the caller's next synchronisation.
+ *   - Calls on different streams may run concurrently.  The GEMM's split-tile
+ *     workspace is owned by the library, one per device and stream.
+ */
+#ifndef COMET_H
+#define COMET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hipStream_t;
+
+typedef enum {
+  COMET_OK = 0,
+  COMET_ERR_INVALID_ARG = 1,
+  COMET_ERR_UNSUPPORTED = 2,
+  COMET_ERR_HIP = 3,
+  COMET_ERR_OOM = 4
+} comet_status_t;
+
+/* Bytes of A_packed for M tokens, K channels, block size G and the given map
+ * (M * sum_g B(p[g])).  Returns 0 for invalid arguments. */
+size_t comet_act_packed_bytes(const uint8_t* group_prec_map, int M, int K, int G);
+
+/* Online FMPQ activation quantization (Sec. 3.2): for every token m and block
+ * g, quantize X[m, gG:(g+1)G] to p[g] bits and write the codes to A_packed and
+ * the scale to a_scales[g][m].
+ *   X        device, fp16 [M][K] row-major, 16-byte aligned.
+ *   A_packed device, comet_act_packed_bytes(...) bytes, 16-byte aligned.
+ *   a_scales device, fp16 [K/G][M].
+ * Non-finite inputs are not supported (the codes they produce are unspecified). */
+comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* group_prec_map,
+                                       uint8_t* A_packed, uint16_t* a_scales, int M, int K,
+                                       int G, hipStream_t stream);
+
+/* Offline 4-bit weight quantization and packing (weights are 4-bit, Sec. 3.2;
+ * stored in the operand layout the GEMM reads, Sec. 4.3).
+ *   W        device, fp16 [N][K] row-major (nn.Linear layout).
+ *   W_packed device, [N][K/2] bytes.
+ *   w_scales device, fp16 [K/G][N]. */
+comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
+                             int K, int G, hipStream_t stream);
+
+/* W4Ax GEMM (Sec. 4, O = WX): out[m][n] = fp16( sum_g a_scales[g][m] *
+ * w_scales[g][n] * sum_{c<G} qa[m][gG+c] * qw[n][gG+c] ).  The per-block sums
+ * are exact; the sum over blocks is fp32 in an unspecified order, rounded once
+ * to fp16 (nearest even).  Output is deterministic for a given build, device,
+ * shape and map.  N must be a multiple of 16. */
+comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* group_prec_map,
+                               const uint16_t* a_scales, const uint8_t* W_packed,
+                               const uint16_t* w_scales, uint16_t* out, int M, int N, int K,
+                               int G, hipStream_t stream);
+
+/* Diagnostic form of the same contraction: writes the exact per-block integer
+ * sums acc[m - m0][n - n0][g] = sum_{c<G} qa[m][gG+c] * qw[n][gG+c] (int32)
+ * for the window m0 <= m < m1, n0 <= n < n1, computed by the GEMM's own
+ * operand path (Sec. 4.1, the integer tile results before dequantization).
+ *   acc device, int32 [m1-m0][n1-n0][K/G]. */
+comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* group_prec_map,
+                                   const uint16_t* a_scales, const uint8_t* W_packed,
+                                   const uint16_t* w_scales, int32_t* acc, int M, int N, int K,
+                                   int G, int m0, int m1, int n0, int n1, hipStream_t stream);
+
+/* Host-only view of the per-block-precision tile schedule (Sec. 4.4: tile
+ * remapping and tile decomposition) that comet_w4ax_gemm would use for this
+ * shape and map on `num_cus` compute units.  Nothing is launched and no device
+ * is touched.  Each work unit is five ints {tile, g_begin, g_end, slot, nslots}:
+ * output tile `tile` (row-major over the tile grid), blocks [g_begin, g_end)
+ * in the schedule's block order, written as partial `slot` of `nslots`
+ * (nslots == 1: the unit owns the whole tile).  Units are listed per
+ * persistent workgroup: wg_begin[w] .. wg_begin[w+1].  Returns the number of
+ * units and workgroups through *n_units / *n_wgs; arrays may be NULL to query
+ * sizes.  order (may be NULL) receives the K/G block order. */
+comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* group_prec_map,
+                                    int num_cus, int* units, int max_units, int* n_units,
+                                    int* wg_begin, int max_wgs, int* n_wgs, int* order,
+                                    int* tile_m, int* tile_n);
+
+const char* comet_status_str(comet_status_t status);
+
+/* Message for the last error on the calling thread ("" if none). */
+const char* comet_last_error(void);
+
+/* Free the library's cached plans and workspaces on every device.  Not to be
+ * called while work the library enqueued is still running. */
+void comet_release_caches(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,208 @@
+"""Python binding of libcomet (include/comet.h): COMET's W4Ax hot path on MI355X.
+
+The functions named like the C entry points pass tensor data pointers, sizes
+and the current HIP stream straight through ctypes; every step of the path
+runs in libcomet's gfx950 kernels.  PyTorch only provides device memory and
+streams.  There is no CPU fallback: if libcomet.so is missing and cannot be
+built, importing a function raises.
+
+Convenience wrappers (``quantize_act``, ``pack_w4``, ``w4ax_gemm``) allocate
+the outputs with ``torch.empty`` and call the same entry points.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcomet.so")
+G = 128
+
+_lib = None
+
+
+class CometError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_status_name(status)}: {message}")
+        self.status = status
+
+
+def _status_name(s: int) -> str:
+    return {0: "COMET_OK", 1: "COMET_ERR_INVALID_ARG", 2: "COMET_ERR_UNSUPPORTED",
+            3: "COMET_ERR_HIP", 4: "COMET_ERR_OOM"}.get(s, f"status {s}")
+
+
+def lib():
+    """The loaded libcomet.so (built in-tree with hipcc if it is not there yet)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        from . import build as _build
+
+        _build.build()
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    sigs = {
+        "comet_act_packed_bytes": (S, [P, I, I, I]),
+        "comet_fmpq_quantize_act": (I, [P, P, P, P, I, I, I, P]),
+        "comet_pack_w4": (I, [P, P, P, I, I, I, P]),
+        "comet_w4ax_gemm": (I, [P, P, P, P, P, P, I, I, I, I, P]),
+        "comet_w4ax_gemm_acc": (I, [P, P, P, P, P, P, I, I, I, I, I, I, I, I, P]),
+        "comet_schedule_query": (I, [I, I, I, I, P, I, P, I, P, P, I, P, P, P, P]),
+        "comet_status_str": (ctypes.c_char_p, [I]),
+        "comet_last_error": (ctypes.c_char_p, []),
+        "comet_release_caches": (None, []),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise CometError(status, lib().comet_last_error().decode())
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    if t is None:
+        return ctypes.c_void_p(0)
+    if isinstance(t, int):
+        return ctypes.c_void_p(t)
+    if isinstance(t, np.ndarray):
+        return ctypes.c_void_p(t.ctypes.data)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        import torch
+
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _map(prec) -> np.ndarray:
+    m = np.ascontiguousarray(np.asarray(prec, dtype=np.uint8))
+    return m
+
+
+# --- the C entry points ----------------------------------------------------------
+
+def comet_act_packed_bytes(group_prec_map, M: int, K: int, G: int = G) -> int:
+    m = _map(group_prec_map)
+    return int(lib().comet_act_packed_bytes(_ptr(m), M, K, G))
+
+
+def comet_fmpq_quantize_act(X, group_prec_map, A_packed, a_scales, M: int, K: int, G: int = G,
+                            stream=None) -> None:
+    m = _map(group_prec_map)
+    _check(lib().comet_fmpq_quantize_act(_ptr(X), _ptr(m), _ptr(A_packed), _ptr(a_scales), M, K,
+                                         G, _stream(stream)))
+
+
+def comet_pack_w4(W, W_packed, w_scales, N: int, K: int, G: int = G, stream=None) -> None:
+    _check(lib().comet_pack_w4(_ptr(W), _ptr(W_packed), _ptr(w_scales), N, K, G,
+                               _stream(stream)))
+
+
+def comet_w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, out, M: int, N: int,
+                    K: int, G: int = G, stream=None) -> None:
+    m = _map(group_prec_map)
+    _check(lib().comet_w4ax_gemm(_ptr(A_packed), _ptr(m), _ptr(a_scales), _ptr(W_packed),
+                                 _ptr(w_scales), _ptr(out), M, N, K, G, _stream(stream)))
+
+
+def comet_w4ax_gemm_acc(A_packed, group_prec_map, a_scales, W_packed, w_scales, acc, M: int,
+                        N: int, K: int, G: int, m0: int, m1: int, n0: int, n1: int,
+                        stream=None) -> None:
+    m = _map(group_prec_map)
+    _check(lib().comet_w4ax_gemm_acc(_ptr(A_packed), _ptr(m), _ptr(a_scales), _ptr(W_packed),
+                                     _ptr(w_scales), _ptr(acc), M, N, K, G, m0, m1, n0, n1,
+                                     _stream(stream)))
+
+
+def comet_schedule_query(M: int, N: int, K: int, group_prec_map, num_cus: int = 256,
+                         G: int = G) -> dict:
+    """Host-only view of the GEMM's tile schedule (no device needed)."""
+    m = _map(group_prec_map)
+    L = lib()
+    nu, nw, tm, tn = ctypes.c_int(), ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(L.comet_schedule_query(M, N, K, G, _ptr(m), num_cus, None, 0, ctypes.byref(nu), None,
+                                  0, ctypes.byref(nw), None, ctypes.byref(tm), ctypes.byref(tn)))
+    units = np.zeros((nu.value, 5), np.int32)
+    wgb = np.zeros(nw.value + 1, np.int32)
+    order = np.zeros(K // G, np.int32)
+    _check(L.comet_schedule_query(M, N, K, G, _ptr(m), num_cus, _ptr(units), nu.value,
+                                  ctypes.byref(nu), _ptr(wgb), nw.value + 1, ctypes.byref(nw),
+                                  _ptr(order), ctypes.byref(tm), ctypes.byref(tn)))
+    return {"units": units, "wg_begin": wgb, "order": order, "tile_m": tm.value,
+            "tile_n": tn.value, "num_wgs": nw.value}
+
+
+def comet_last_error() -> str:
+    return lib().comet_last_error().decode()
+
+
+def comet_status_str(status: int) -> str:
+    return lib().comet_status_str(status).decode()
+
+
+def comet_release_caches() -> None:
+    lib().comet_release_caches()
+
+
+# --- allocating conveniences (torch tensors on the current device) ----------------
+
+def quantize_act(X, group_prec_map, stream=None):
+    """X: float16 [M][K] CUDA tensor -> (A_packed uint8, a_scales float16 [K/G][M])."""
+    import torch
+
+    M, K = X.shape
+    nbytes = comet_act_packed_bytes(group_prec_map, M, K)
+    if nbytes == 0:
+        raise CometError(1, "invalid map or shape")
+    A = torch.empty(nbytes, dtype=torch.uint8, device=X.device)
+    sa = torch.empty((K // G, M), dtype=torch.float16, device=X.device)
+    comet_fmpq_quantize_act(X, group_prec_map, A, sa, M, K, G, stream)
+    return A, sa
+
+
+def pack_w4(W, stream=None):
+    """W: float16 [N][K] CUDA tensor -> (W_packed uint8 [N][K/2], w_scales float16 [K/G][N])."""
+    import torch
+
+    N, K = W.shape
+    Wp = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
+    sw = torch.empty((K // G, N), dtype=torch.float16, device=W.device)
+    comet_pack_w4(W, Wp, sw, N, K, G, stream)
+    return Wp, sw
+
+
+def w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int, N: int, K: int,
+              out=None, stream=None):
+    import torch
+
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=A_packed.device)
+    comet_w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, out, M, N, K, G,
+                    stream)
+    return out
+
+
+def w4ax_gemm_acc(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int, N: int, K: int,
+                  m0: int, m1: int, n0: int, n1: int, stream=None):
+    import torch
+
+    acc = torch.empty((m1 - m0, n1 - n0, K // G), dtype=torch.int32, device=A_packed.device)
+    comet_w4ax_gemm_acc(A_packed, group_prec_map, a_scales, W_packed, w_scales, acc, M, N, K, G,
+                        m0, m1, n0, n1, stream)
+    return acc

@@ -1,0 +1,282 @@
+// comet_api.cpp -- the C ABI of libcomet (include/comet.h): argument checks,
+// device checks, plan cache and kernel launches.  Every step of the path runs
+// in the HIP kernels; this file only validates, plans and enqueues.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/comet.h"
+#include "kernels.h"
+#include "scheduler.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+comet_status_t fail(comet_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+comet_status_t ok() {
+  g_last_error.clear();
+  return COMET_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Checks shared by every entry point: G, K and the block map.
+comet_status_t check_kg(int K, int G) {
+  if (G != comet::kG) return fail(COMET_ERR_UNSUPPORTED, "G=%d: only G=128 is supported", G);
+  if (K < G || K % G) return fail(COMET_ERR_INVALID_ARG, "K=%d must be a positive multiple of G", K);
+  if (K / G > comet::kMaxBlocks)
+    return fail(COMET_ERR_UNSUPPORTED, "K=%d exceeds %d", K, comet::kMaxBlocks * comet::kG);
+  return COMET_OK;
+}
+
+comet_status_t make_map(const uint8_t* prec, int NG, comet::BlockMap* map) {
+  if (!prec) return fail(COMET_ERR_INVALID_ARG, "group_prec_map is null");
+  std::memset(map, 0, sizeof *map);
+  for (int g = 0; g < NG; ++g) {
+    if (prec[g] == 8)
+      map->bits[g >> 6] |= 1ull << (g & 63);
+    else if (prec[g] != 4)
+      return fail(COMET_ERR_INVALID_ARG, "group_prec_map[%d]=%d is not 4 or 8", g, (int)prec[g]);
+  }
+  return COMET_OK;
+}
+
+struct DeviceInfo {
+  bool gfx950 = false;
+  int cus = 0;
+};
+
+std::mutex g_mu;
+std::map<int, DeviceInfo> g_devices;
+
+// Current device, checked to be gfx950.  COMET_TEST_FORCE_ARCH replaces the
+// reported architecture name (used by the CPU tests of this check).
+comet_status_t current_device(int* dev, DeviceInfo* info) {
+  const char* forced = std::getenv("COMET_TEST_FORCE_ARCH");
+  if (forced && *forced) {
+    if (std::strncmp(forced, "gfx950", 6) != 0)
+      return fail(COMET_ERR_UNSUPPORTED, "device architecture %s is not gfx950", forced);
+  }
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return fail(COMET_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_devices.find(*dev);
+  if (it == g_devices.end()) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, *dev);
+    if (e != hipSuccess)
+      return fail(COMET_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+    DeviceInfo di;
+    di.gfx950 = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    di.cus = prop.multiProcessorCount;
+    it = g_devices.emplace(*dev, di).first;
+  }
+  *info = it->second;
+  if (!info->gfx950) return fail(COMET_ERR_UNSUPPORTED, "current device is not gfx950");
+  return COMET_OK;
+}
+
+comet_status_t launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(COMET_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* comet_status_str(comet_status_t s) {
+  switch (s) {
+    case COMET_OK: return "COMET_OK";
+    case COMET_ERR_INVALID_ARG: return "COMET_ERR_INVALID_ARG";
+    case COMET_ERR_UNSUPPORTED: return "COMET_ERR_UNSUPPORTED";
+    case COMET_ERR_HIP: return "COMET_ERR_HIP";
+    case COMET_ERR_OOM: return "COMET_ERR_OOM";
+  }
+  return "COMET_ERR_UNKNOWN";
+}
+
+const char* comet_last_error(void) { return g_last_error.c_str(); }
+
+size_t comet_act_packed_bytes(const uint8_t* prec, int M, int K, int G) {
+  if (!prec || M < 1 || G < 1 || K < G || K % G) return 0;
+  size_t units = 0;
+  for (int g = 0; g < K / G; ++g) {
+    if (prec[g] != 4 && prec[g] != 8) return 0;
+    units += prec[g] == 8 ? (size_t)G : (size_t)G / 2;
+  }
+  return units * (size_t)M;
+}
+
+comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* prec, uint8_t* A_packed,
+                                       uint16_t* a_scales, int M, int K, int G,
+                                       hipStream_t stream) {
+  if (!X || !A_packed || !a_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (M < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d must be >= 1", M);
+  comet_status_t st = check_kg(K, G);
+  if (st) return st;
+  if (!aligned16(X) || !aligned16(A_packed) || !aligned16(a_scales))
+    return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  comet::BlockMap map;
+  if ((st = make_map(prec, K / G, &map))) return st;
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  return launched(comet::launch_quantize_act(X, A_packed, a_scales, M, K, map, stream),
+                  "quantize_act launch");
+}
+
+comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
+                             int K, int G, hipStream_t stream) {
+  if (!W || !W_packed || !w_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (N < 1) return fail(COMET_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+  comet_status_t st = check_kg(K, G);
+  if (st) return st;
+  if (!aligned16(W) || !aligned16(W_packed) || !aligned16(w_scales))
+    return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  return launched(comet::launch_pack_w4(W, W_packed, w_scales, N, K, stream), "pack_w4 launch");
+}
+
+static comet_status_t gemm_common(const uint8_t* A, const uint8_t* prec, const uint16_t* sa,
+                                  const uint8_t* W, const uint16_t* sw, void* out, int M, int N,
+                                  int K, int G, comet::BlockMap* map) {
+  if (!A || !sa || !W || !sw || !out) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (M < 1 || N < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d, N=%d must be >= 1", M, N);
+  if (N % 16) return fail(COMET_ERR_INVALID_ARG, "N=%d must be a multiple of 16", N);
+  comet_status_t st = check_kg(K, G);
+  if (st) return st;
+  if (!aligned16(A) || !aligned16(sa) || !aligned16(W) || !aligned16(sw) || !aligned16(out))
+    return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  return make_map(prec, K / G, map);
+}
+
+comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* prec,
+                               const uint16_t* a_scales, const uint8_t* W_packed,
+                               const uint16_t* w_scales, uint16_t* out, int M, int N, int K,
+                               int G, hipStream_t stream) {
+  comet::BlockMap map;
+  comet_status_t st =
+      gemm_common(A_packed, prec, a_scales, W_packed, w_scales, out, M, N, K, G, &map);
+  if (st) return st;
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  comet::GemmArgs a{};
+  a.A = A_packed;
+  a.sa = a_scales;
+  a.W = W_packed;
+  a.sw = w_scales;
+  a.out = out;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.tiles_n = (N + comet::kTileN - 1) / comet::kTileN;
+  a.map = map;
+  return launched(comet::launch_gemm_simple(a, false, stream), "gemm launch");
+}
+
+comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* prec,
+                                   const uint16_t* a_scales, const uint8_t* W_packed,
+                                   const uint16_t* w_scales, int32_t* acc, int M, int N, int K,
+                                   int G, int m0, int m1, int n0, int n1, hipStream_t stream) {
+  comet::BlockMap map;
+  comet_status_t st =
+      gemm_common(A_packed, prec, a_scales, W_packed, w_scales, acc, M, N, K, G, &map);
+  if (st) return st;
+  if (m0 < 0 || m1 > M || m0 >= m1 || n0 < 0 || n1 > N || n0 >= n1)
+    return fail(COMET_ERR_INVALID_ARG, "window [%d,%d)x[%d,%d) is empty or outside %dx%d", m0,
+                m1, n0, n1, M, N);
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  comet::GemmArgs a{};
+  a.A = A_packed;
+  a.sa = a_scales;
+  a.W = W_packed;
+  a.sw = w_scales;
+  a.acc = acc;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.tiles_n = (N + comet::kTileN - 1) / comet::kTileN;
+  a.win_m0 = m0;
+  a.win_m1 = m1;
+  a.win_n0 = n0;
+  a.win_n1 = n1;
+  a.map = map;
+  return launched(comet::launch_gemm_simple(a, true, stream), "gemm_acc launch");
+}
+
+comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* prec, int num_cus,
+                                    int* units, int max_units, int* n_units, int* wg_begin,
+                                    int max_wgs, int* n_wgs, int* order, int* tile_m,
+                                    int* tile_n) {
+  if (M < 1 || N < 1 || num_cus < 1) return fail(COMET_ERR_INVALID_ARG, "bad shape or CU count");
+  comet_status_t st = check_kg(K, G);
+  if (st) return st;
+  comet::BlockMap map;
+  if ((st = make_map(prec, K / G, &map))) return st;
+  comet::PlanOptions opt;
+  opt.num_cus = num_cus;
+  const char* mode = std::getenv("COMET_SCHED");
+  if (mode && *mode) opt.mode = mode;
+  comet::Plan plan;
+  std::string err;
+  if (!comet::build_plan(M, N, K, G, prec, opt, &plan, &err))
+    return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
+  if (n_units) *n_units = (int)plan.units.size();
+  if (n_wgs) *n_wgs = plan.num_wgs;
+  if (tile_m) *tile_m = plan.tile_m;
+  if (tile_n) *tile_n = plan.tile_n;
+  if (units) {
+    if (max_units < (int)plan.units.size())
+      return fail(COMET_ERR_INVALID_ARG, "units buffer holds %d, need %d", max_units,
+                  (int)plan.units.size());
+    for (size_t i = 0; i < plan.units.size(); ++i) {
+      const comet::PlanUnit& u = plan.units[i];
+      int* o = units + 5 * i;
+      o[0] = u.tile;
+      o[1] = u.g_begin;
+      o[2] = u.g_end;
+      o[3] = u.slot;
+      o[4] = u.nslots;
+    }
+  }
+  if (wg_begin) {
+    if (max_wgs < plan.num_wgs + 1)
+      return fail(COMET_ERR_INVALID_ARG, "wg_begin buffer holds %d, need %d", max_wgs,
+                  plan.num_wgs + 1);
+    for (int i = 0; i <= plan.num_wgs; ++i) wg_begin[i] = plan.wg_begin[i];
+  }
+  if (order)
+    for (int i = 0; i < K / G; ++i) order[i] = plan.order[i];
+  return ok();
+}
+
+void comet_release_caches(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_devices.clear();
+}
+
+}  // extern "C"

@@ -1,0 +1,59 @@
+// kernels.h -- internal launchers of libcomet's gfx950 kernels (not part of
+// the public C ABI; see include/comet.h for that).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace comet {
+
+constexpr int kG = 128;          // block size along K (the paper's k = 128)
+constexpr int kMaxBlocks = 512;  // blocks per row supported by the bit map (K <= 65536)
+
+// Precision of every K-block as a bit set (bit g = 1: block g is 8-bit),
+// passed by value as a kernel argument so no device table is needed.
+struct BlockMap {
+  uint64_t bits[kMaxBlocks / 64];
+};
+
+// One unit of GEMM work: blocks [g_begin, g_end) (positions in the schedule's
+// block order) of output tile `tile`, written as partial `slot` of `nslots`.
+struct WorkUnit {
+  int tile;
+  int g_begin;
+  int g_end;
+  int slot;
+  int nslots;
+};
+
+struct GemmArgs {
+  const uint8_t* A;
+  const uint16_t* sa;
+  const uint8_t* W;
+  const uint16_t* sw;
+  uint16_t* out;
+  int32_t* acc;       // diagnostic window output (or null)
+  float* partials;    // split-tile fp32 partials [tile slot][TM*TN]
+  int* counters;      // per split tile arrival counters (zero between launches)
+  const WorkUnit* units;
+  const int* wg_begin;
+  const int* order;   // K-block order, K/G entries
+  const int* split_index;  // tile -> index into the partial/counter arrays (-1: not split)
+  int M, N, K;
+  int tiles_n;        // tiles along N
+  int win_m0, win_m1, win_n0, win_n1;
+  BlockMap map;
+};
+
+hipError_t launch_quantize_act(const uint16_t* X, uint8_t* A, uint16_t* sa, int M, int K,
+                               const BlockMap& map, hipStream_t stream);
+hipError_t launch_pack_w4(const uint16_t* W, uint8_t* Wp, uint16_t* sw, int N, int K,
+                          hipStream_t stream);
+
+// Output-tile edge of the GEMM kernels.
+constexpr int kTileM = 128;
+constexpr int kTileN = 128;
+
+hipError_t launch_gemm_simple(const GemmArgs& a, bool diag, hipStream_t stream);
+
+}  // namespace comet

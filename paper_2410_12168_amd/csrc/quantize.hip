@@ -1,0 +1,176 @@
+// quantize.hip -- fused block quantize + pack kernels for gfx950.
+//
+// FMPQ (paper Sec. 3.2): every token's activations are split into blocks of
+// G = 128 channels; each block is quantized symmetrically to 4 or 8 bits with
+// one fp16 scale.  The same block quantizer packs the 4-bit weights offline.
+//
+// Work decomposition: 16 lanes own one (row, block) pair, 8 channels per lane
+// (one 128-bit load of fp16).  The 16-lane max reduction stays inside a DPP
+// row.  Each lane then emits one packed dword (4-bit) or two (8-bit), so a
+// wave writes 256 B (4-bit) or 512 B (8-bit) of contiguous packed output.
+// The kernels are HBM-bound: 2 bytes in per channel, 0.5 or 1 byte out.
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+#include "kernels.h"
+
+namespace comet {
+
+namespace {
+
+struct Codes {
+  uint32_t sign[8];
+  uint32_t mag[8];
+};
+
+// Quantize the 8 channels this lane holds, given the block-wide max |x|.
+// Scale and codes follow the block quantizer exactly: one IEEE fp32 division
+// for the scale, rounding to binary16 (nearest even), then one IEEE fp32
+// division per element, rint (nearest even) and clamp.
+__device__ inline uint16_t quantize8(const float (&x)[8], float amax, int qmax, Codes& c) {
+  float s32 = amax / (float)qmax;
+  __half h = __float2half_rn(s32);
+  float s = __half2float(h);
+  #pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float r = 0.0f;
+    if (s != 0.0f) {
+      r = rintf(x[i] / s);
+      r = fminf(fmaxf(r, (float)-qmax), (float)qmax);
+    }
+    int q = (int)r;
+    c.sign[i] = q < 0 ? 1u : 0u;
+    c.mag[i] = (uint32_t)(q < 0 ? -q : q);
+  }
+  return __half_as_ushort(h);
+}
+
+// Sign-magnitude 4-bit codes of channels 0..7 into one dword.  Byte k:
+//   bit 7 = sign(k), bits 6..4 = |code 4+k|, bit 3 = sign(4+((k+3)&3)), bits 2..0 = |code k|,
+// so that (w & 0x87878787) and (rotr(w, 4) & 0x87878787) are FP8-E4M3 subnormals.
+__device__ inline uint32_t pack4(const Codes& c) {
+  uint32_t w = 0;
+  #pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint32_t b = (c.sign[k] << 7) | (c.mag[4 + k] << 4) | (c.sign[4 + ((k + 3) & 3)] << 3) | c.mag[k];
+    w |= b << (8 * k);
+  }
+  return w;
+}
+
+__device__ inline uint2 pack8(const Codes& c) {
+  uint32_t w0 = 0, w1 = 0;
+  #pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    w0 |= ((c.sign[k] << 7) | c.mag[k]) << (8 * k);
+    w1 |= ((c.sign[4 + k] << 7) | c.mag[4 + k]) << (8 * k);
+  }
+  return make_uint2(w0, w1);
+}
+
+__device__ inline void load8(const uint16_t* p, float (&x)[8]) {
+  uint4 v = *reinterpret_cast<const uint4*>(p);
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  #pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __half2float(__ushort_as_half((unsigned short)(w[i] & 0xFFFF)));
+    x[2 * i + 1] = __half2float(__ushort_as_half((unsigned short)(w[i] >> 16)));
+  }
+}
+
+__device__ inline float max16(float v) {
+  // butterfly over the 16 lanes of one (row, block) pair
+  v = fmaxf(v, __shfl_xor(v, 1, 16));
+  v = fmaxf(v, __shfl_xor(v, 2, 16));
+  v = fmaxf(v, __shfl_xor(v, 4, 16));
+  v = fmaxf(v, __shfl_xor(v, 8, 16));
+  return v;
+}
+
+__device__ inline int n8_before(const BlockMap& map, int g) {
+  int n = 0;
+  for (int w = 0; w < (g >> 6); ++w) n += __popcll(map.bits[w]);
+  if (g & 63) n += __popcll(map.bits[g >> 6] & ((1ull << (g & 63)) - 1));
+  return n;
+}
+
+// Activations: pair p -> (block g = p / M, row m = p % M), so the pairs of one
+// workgroup are consecutive rows of one block and their packed outputs are
+// contiguous in the block-major A_packed.
+__global__ __launch_bounds__(256) void quantize_act_kernel(const uint16_t* __restrict__ X,
+                                                           uint8_t* __restrict__ A,
+                                                           uint16_t* __restrict__ sa, int M,
+                                                           int K, long long npairs, BlockMap map) {
+  const int lane16 = threadIdx.x & 15;
+  const long long p = (long long)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const bool valid = p < npairs;
+  const long long pc = valid ? p : npairs - 1;
+  const int g = (int)(pc / M);
+  const int m = (int)(pc % M);
+  const bool b8 = (map.bits[g >> 6] >> (g & 63)) & 1;
+  float x[8];
+  load8(X + (size_t)m * K + (size_t)g * kG + 8 * lane16, x);
+  float a = 0.0f;
+  #pragma unroll
+  for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
+  a = max16(a);
+  Codes c;
+  uint16_t s16 = quantize8(x, a, b8 ? 127 : 7, c);
+  if (!valid) return;
+  const size_t base = (size_t)M * 64 * (size_t)(g + n8_before(map, g));
+  if (b8) {
+    *reinterpret_cast<uint2*>(A + base + (size_t)m * 128 + 8 * lane16) = pack8(c);
+  } else {
+    *reinterpret_cast<uint32_t*>(A + base + (size_t)m * 64 + 4 * lane16) = pack4(c);
+  }
+  if (lane16 == 0) sa[(size_t)g * M + m] = s16;
+}
+
+// Weights: pair p -> (row n = p / NG, block g = p % NG); consecutive pairs are
+// consecutive blocks of one row, contiguous in the row-major W_packed.
+__global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t* __restrict__ W,
+                                                      uint8_t* __restrict__ Wp,
+                                                      uint16_t* __restrict__ sw, int N, int K,
+                                                      long long npairs) {
+  const int lane16 = threadIdx.x & 15;
+  const long long p = (long long)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const bool valid = p < npairs;
+  const long long pc = valid ? p : npairs - 1;
+  const int NG = K / kG;
+  const int n = (int)(pc / NG);
+  const int g = (int)(pc % NG);
+  float x[8];
+  load8(W + (size_t)n * K + (size_t)g * kG + 8 * lane16, x);
+  float a = 0.0f;
+  #pragma unroll
+  for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
+  a = max16(a);
+  Codes c;
+  uint16_t s16 = quantize8(x, a, 7, c);
+  if (!valid) return;
+  *reinterpret_cast<uint32_t*>(Wp + (size_t)n * (K / 2) + (size_t)g * 64 + 4 * lane16) = pack4(c);
+  if (lane16 == 0) sw[(size_t)g * N + n] = s16;
+}
+
+}  // namespace
+
+hipError_t launch_quantize_act(const uint16_t* X, uint8_t* A, uint16_t* sa, int M, int K,
+                               const BlockMap& map, hipStream_t stream) {
+  long long npairs = (long long)M * (K / kG);
+  long long blocks = (npairs + 15) / 16;
+  hipLaunchKernelGGL(quantize_act_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, X, A, sa,
+                     M, K, npairs, map);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_w4(const uint16_t* W, uint8_t* Wp, uint16_t* sw, int N, int K,
+                          hipStream_t stream) {
+  long long npairs = (long long)N * (K / kG);
+  long long blocks = (npairs + 15) / 16;
+  hipLaunchKernelGGL(pack_w4_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, W, Wp, sw, N,
+                     K, npairs);
+  return hipGetLastError();
+}
+
+}  // namespace comet

@@ -1,0 +1,86 @@
+"""Properties of the per-block-precision tile scheduler (host only).
+
+Tile remapping and tile decomposition (paper Sec. 4.4) must cover every
+(tile, K-block) pair exactly once, number the partial slots of split tiles
+consistently, keep every workgroup's cost within one K-block of the mean,
+and be deterministic.
+"""
+import numpy as np
+import pytest
+
+import paper_2410_12168_amd as comet
+import synth
+
+COST4, COST8 = 1.0, 1.6
+
+
+def check_plan(M, N, K, prec, num_cus=256):
+    s = comet.comet_schedule_query(M, N, K, prec, num_cus)
+    NG = K // 128
+    tm, tn = s["tile_m"], s["tile_n"]
+    T = -(-M // tm) * -(-N // tn)
+    order = s["order"]
+    assert sorted(order.tolist()) == list(range(NG))  # a permutation
+    p = np.asarray(prec)[order]
+    assert np.all(np.diff((p == 8).astype(int)) >= 0)  # 4-bit blocks first, then 8-bit
+    cover = np.zeros((T, NG), np.int32)
+    slots = {}
+    units, wgb = s["units"], s["wg_begin"]
+    assert wgb[0] == 0 and wgb[-1] == len(units) and np.all(np.diff(wgb) >= 0)
+    assert s["num_wgs"] <= num_cus
+    cost = np.where(p == 8, COST8, COST4)
+    prefix = np.concatenate([[0], np.cumsum(cost)])
+    wg_cost = []
+    for w in range(s["num_wgs"]):
+        c = 0.0
+        for tile, g0, g1, slot, ns in units[wgb[w]:wgb[w + 1]]:
+            assert 0 <= tile < T and 0 <= g0 < g1 <= NG and 0 <= slot < ns
+            cover[tile, g0:g1] += 1
+            slots.setdefault(tile, []).append((slot, ns, g0, g1))
+            c += prefix[g1] - prefix[g0]
+        wg_cost.append(c)
+    assert np.all(cover == 1)  # every (tile, block) exactly once
+    for tile, ss in slots.items():
+        ns = ss[0][1]
+        assert all(x[1] == ns for x in ss) and sorted(x[0] for x in ss) == list(range(ns))
+        # slots follow the block order
+        assert [x[2] for x in sorted(ss)] == sorted(x[2] for x in ss)
+    wg_cost = np.array(wg_cost)
+    return s, wg_cost, prefix[-1]
+
+
+@pytest.mark.parametrize("M,N,K", [(2048, 6144, 4096), (2048, 4096, 4096), (2048, 28672, 4096),
+                                   (2048, 4096, 14336), (4096, 10240, 8192), (4096, 8192, 8192),
+                                   (4096, 57344, 8192), (4096, 8192, 28672), (16, 1024, 1024),
+                                   (1, 57344, 8192), (128, 57344, 8192), (100, 272, 1152)])
+def test_cover_and_balance(M, N, K):
+    NG = K // 128
+    prec = synth.prec_map(NG, max(1, NG // 16))
+    s, wg_cost, Ct = check_plan(M, N, K, prec)
+    T = -(-M // s["tile_m"]) * -(-N // s["tile_n"])
+    if T > 256:
+        # balanced: no workgroup above the mean by more than one 8-bit block
+        assert wg_cost.max() <= wg_cost.mean() + COST8 + 1e-9
+
+
+@pytest.mark.parametrize("frac", [0, 1 / 16, 1 / 4, 1 / 2])
+@pytest.mark.parametrize("placement", ["contiguous", "random"])
+def test_load_balance_sweep(frac, placement):
+    K = 28672
+    NG = K // 128
+    prec = synth.prec_map(NG, int(NG * frac), placement, seed=1)
+    s, wg_cost, Ct = check_plan(4096, 8192, K, prec)
+    assert wg_cost.max() <= wg_cost.mean() + COST8 + 1e-9
+
+
+def test_deterministic():
+    prec = synth.prec_map(64, 4, "random", 3)
+    a = comet.comet_schedule_query(4096, 10240, 8192, prec)
+    b = comet.comet_schedule_query(4096, 10240, 8192, prec)
+    assert all(np.array_equal(a[k], b[k]) for k in ("units", "wg_begin", "order"))
+
+
+def test_small_cu_counts():
+    prec = synth.prec_map(8, 1)
+    for cus in (1, 3, 7, 64):
+        check_plan(300, 1024, 1024, prec, num_cus=cus)
