@@ -1,0 +1,219 @@
+"""Benchmark of the W4Ax hot path on one MI355X.
+
+One step = the whole hot path over one batch: for each linear layer of the
+workload, online FMPQ quantization of the fp16 activations (M tokens) and the
+W4Ax GEMM against the layer's pre-packed 4-bit weights.  Weight packing is
+offline (done once before timing).  Inputs are seeded synthetic tensors of the
+layer shapes, resident in HBM before the timed region starts.
+
+Prints ONE JSON line.  ``value`` is effective TOPS = sum over layers of
+2*M*N*K divided by the step time.  ``roofline`` describes the GEMM kernel
+(ops per launch over its average launch time, measured with HIP events on the
+stream the kernels run on).  ``cpu_baseline`` times the CPU oracle on a
+bounded sample of the same workload (a few token rows of every layer) and also
+checks the GPU output rows of that sample against it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+PEAK_MFMA_TFLOPS = 5000.0  # MI355X dense FP8 (= dense INT8) MFMA
+PEAK_HBM_GBS = 8000.0
+
+WORKLOADS = {
+    "llama3-70b-prefill": dict(M=4096, layers="LLAMA3_70B"),
+    "llama3-8b-prefill": dict(M=2048, layers="LLAMA3_8B"),
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama3-70b-prefill", choices=sorted(WORKLOADS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--frac8", type=float, default=1 / 16)
+    ap.add_argument("--cpu-rows", type=int, default=512,
+                    help="token rows per layer in the CPU-oracle sample (0: skip)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the W4Ax GEMM is a single-GPU kernel and this "
+              "build has no multi-GPU path (--gpus must be 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2410_12168_amd as comet
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = WORKLOADS[args.workload]
+    M = wl["M"]
+    shapes = getattr(synth, wl["layers"])
+    layers = []
+    t_setup = time.time()
+    for name, (K, N) in shapes.items():
+        NG = K // 128
+        n8 = int(round(NG * args.frac8))
+        prec = synth.prec_map(NG, n8)
+        X16 = synth.activations(args.seed, M, K, prec)
+        W16 = synth.weights(args.seed, N, K)
+        X = torch.from_numpy(X16.view(np.int16)).to(dev).view(torch.float16)
+        Wd = torch.from_numpy(W16.view(np.int16)).to(dev).view(torch.float16)
+        Wp, sw = comet.pack_w4(Wd)
+        torch.cuda.synchronize()
+        del Wd
+        nbytes = comet.comet_act_packed_bytes(prec, M, K)
+        A = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        sa = torch.empty((NG, M), dtype=torch.float16, device=dev)
+        out = torch.empty((M, N), dtype=torch.float16, device=dev)
+        layers.append(dict(name=name, M=M, N=N, K=K, prec=prec, X=X, X16=X16, W16=W16, Wp=Wp,
+                           sw=sw, A=A, sa=sa, out=out, n8=n8))
+    t_setup = time.time() - t_setup
+
+    def step(ev=None):
+        for i, L in enumerate(layers):
+            if ev is not None:
+                ev[i][0].record()
+            comet.comet_fmpq_quantize_act(L["X"], L["prec"], L["A"], L["sa"], L["M"], L["K"])
+            if ev is not None:
+                ev[i][1].record()
+            comet.comet_w4ax_gemm(L["A"], L["prec"], L["sa"], L["Wp"], L["sw"], L["out"], L["M"],
+                                  L["N"], L["K"])
+            if ev is not None:
+                ev[i][2].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: whole steps
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_per_step = ms_total / args.steps
+
+    # per-kernel launch durations (events around each launch, same stream)
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    q_ms = np.zeros(len(layers))
+    g_ms = np.zeros(len(layers))
+    for s in range(args.steps):
+        for i in range(len(layers)):
+            q_ms[i] += evs[s][i][0].elapsed_time(evs[s][i][1])
+            g_ms[i] += evs[s][i][1].elapsed_time(evs[s][i][2])
+    q_ms /= args.steps
+    g_ms /= args.steps
+
+    ops = np.array([2.0 * L["M"] * L["N"] * L["K"] for L in layers])
+    value = float(ops.sum() / (ms_per_step * 1e-3) / 1e12)
+    achieved = float(ops.sum() / (g_ms.sum() * 1e-3) / 1e12)
+    per_layer = {}
+    for i, L in enumerate(layers):
+        K, N = L["K"], L["N"]
+        NG = K // 128
+        k8 = L["n8"] * 128
+        qbytes = 2 * M * K + M * ((K - k8) // 2 + k8) + 2 * M * NG
+        per_layer[L["name"]] = {
+            "K": K, "N": N, "gemm_us": round(g_ms[i] * 1e3, 2),
+            "gemm_tops": round(ops[i] / (g_ms[i] * 1e-3) / 1e12, 1),
+            "gemm_frac_peak": round(ops[i] / (g_ms[i] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+            "quant_us": round(q_ms[i] * 1e3, 2),
+            "quant_gbs": round(qbytes / (q_ms[i] * 1e-3) / 1e9, 1),
+        }
+
+    record = {
+        "metric": "W4Ax GEMM effective TOPS (LLaMA-3-70B prefill linear layers)",
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: quantize+W4Ax GEMM of qkv/o/gate_up/down at M={M} "
+                        f"tokens, G=128, {args.frac8:.4g} of activation blocks 8-bit",
+            "M": M, "G": 128, "frac8": args.frac8, "seed": args.seed,
+            "operands": "int4 weights, int4/int8 activation codes on FP8-E4M3 MFMA, fp32 dequant",
+        },
+        "roofline": {
+            "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_MFMA_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": None,
+            "kernel": "w4ax_gemm (ops-weighted over the four layer launches)",
+        },
+        "layers": per_layer,
+        "setup_s": round(t_setup, 1),
+    }
+
+    if args.cpu_rows > 0:
+        record["cpu_baseline"] = cpu_baseline(layers, args.cpu_rows)
+
+    print(json.dumps(record), flush=True)
+
+
+def cpu_baseline(layers, rows_per_layer: int) -> dict:
+    """Time the CPU oracle on a bounded sample (the first rows of every layer)
+    and check the GPU output of those rows against it."""
+    import torch
+
+    import oracle
+    from parity import out_errors
+
+    threads = os.cpu_count() or 1
+    rows = np.arange(rows_per_layer)
+    t_total = 0.0
+    ops = 0.0
+    worst = 0.0
+    worst_norm = 0.0
+    for L in layers:
+        qw, sw = oracle.quantize_weight(L["W16"], nthreads=threads)  # offline step, not timed
+        t0 = time.perf_counter()
+        qa, sa = oracle.quantize_act(L["X16"][rows], L["prec"], nthreads=threads)
+        ref = oracle.dequant_gemm(qa, sa, qw, sw, nthreads=threads)
+        t_total += time.perf_counter() - t0
+        ops += 2.0 * len(rows) * L["N"] * L["K"]
+        y = L["out"][: len(rows)].view(torch.int16).cpu().numpy().view(np.float16)
+        mx, norm = out_errors(y, ref)
+        worst = max(worst, mx)
+        worst_norm = max(worst_norm, norm)
+    return {
+        "value": round(ops / t_total / 1e12, 5), "unit": "TOPS", "cores": threads,
+        "kind": "oracle", "seconds": round(t_total, 2),
+        "sample": f"first {rows_per_layer} token rows of each layer (quantize + fp64-dequant GEMM)",
+        "parity_max_rel": worst, "parity_norm_rel": worst_norm, "parity_ok": worst <= 2e-3,
+    }
+
+
+if __name__ == "__main__":
+    main()

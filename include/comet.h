@@ -62,6 +62,12 @@
 extern "C" {
 #endif
 
+#if defined(__GNUC__)
+#define COMET_API __attribute__((visibility("default")))
+#else
+#define COMET_API
+#endif
+
 typedef struct ihipStream_t* hipStream_t;
 
 typedef enum {
@@ -74,7 +80,7 @@ typedef enum {
 
 /* Bytes of A_packed for M tokens, K channels, block size G and the given map
  * (M * sum_g B(p[g])).  Returns 0 for invalid arguments. */
-size_t comet_act_packed_bytes(const uint8_t* group_prec_map, int M, int K, int G);
+COMET_API size_t comet_act_packed_bytes(const uint8_t* group_prec_map, int M, int K, int G);
 
 /* Online FMPQ activation quantization (Sec. 3.2): for every token m and block
  * g, quantize X[m, gG:(g+1)G] to p[g] bits and write the codes to A_packed and
@@ -83,7 +89,7 @@ size_t comet_act_packed_bytes(const uint8_t* group_prec_map, int M, int K, int G
  *   A_packed device, comet_act_packed_bytes(...) bytes, 16-byte aligned.
  *   a_scales device, fp16 [K/G][M].
  * Non-finite inputs are not supported (the codes they produce are unspecified). */
-comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* group_prec_map,
+COMET_API comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* group_prec_map,
                                        uint8_t* A_packed, uint16_t* a_scales, int M, int K,
                                        int G, hipStream_t stream);
 
@@ -92,7 +98,7 @@ comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* group_p
  *   W        device, fp16 [N][K] row-major (nn.Linear layout).
  *   W_packed device, [N][K/2] bytes.
  *   w_scales device, fp16 [K/G][N]. */
-comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
+COMET_API comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
                              int K, int G, hipStream_t stream);
 
 /* W4Ax GEMM (Sec. 4, O = WX): out[m][n] = fp16( sum_g a_scales[g][m] *
@@ -100,7 +106,7 @@ comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_s
  * are exact; the sum over blocks is fp32 in an unspecified order, rounded once
  * to fp16 (nearest even).  Output is deterministic for a given build, device,
  * shape and map.  N must be a multiple of 16. */
-comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* group_prec_map,
+COMET_API comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* group_prec_map,
                                const uint16_t* a_scales, const uint8_t* W_packed,
                                const uint16_t* w_scales, uint16_t* out, int M, int N, int K,
                                int G, hipStream_t stream);
@@ -110,7 +116,7 @@ comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* group_pre
  * for the window m0 <= m < m1, n0 <= n < n1, computed by the GEMM's own
  * operand path (Sec. 4.1, the integer tile results before dequantization).
  *   acc device, int32 [m1-m0][n1-n0][K/G]. */
-comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* group_prec_map,
+COMET_API comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* group_prec_map,
                                    const uint16_t* a_scales, const uint8_t* W_packed,
                                    const uint16_t* w_scales, int32_t* acc, int M, int N, int K,
                                    int G, int m0, int m1, int n0, int n1, hipStream_t stream);
@@ -125,19 +131,19 @@ comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* group
  * persistent workgroup: wg_begin[w] .. wg_begin[w+1].  Returns the number of
  * units and workgroups through *n_units / *n_wgs; arrays may be NULL to query
  * sizes.  order (may be NULL) receives the K/G block order. */
-comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* group_prec_map,
+COMET_API comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* group_prec_map,
                                     int num_cus, int* units, int max_units, int* n_units,
                                     int* wg_begin, int max_wgs, int* n_wgs, int* order,
                                     int* tile_m, int* tile_n);
 
-const char* comet_status_str(comet_status_t status);
+COMET_API const char* comet_status_str(comet_status_t status);
 
 /* Message for the last error on the calling thread ("" if none). */
-const char* comet_last_error(void);
+COMET_API const char* comet_last_error(void);
 
 /* Free the library's cached plans and workspaces on every device.  Not to be
  * called while work the library enqueued is still running. */
-void comet_release_caches(void);
+COMET_API void comet_release_caches(void);
 
 #ifdef __cplusplus
 }

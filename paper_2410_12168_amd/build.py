@@ -17,7 +17,11 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["quantize.hip", "gemm.hip", "scheduler.cpp", "comet_api.cpp"]
 
-COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off",
+# The GEMM's inner loop interleaves MFMAs with the dequantization FMAs: keep
+# MFMA results in VGPRs (no accumulator-register copies).
+PER_FILE = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off", "-fvisibility=hidden",
           "-I" + os.path.join(os.path.dirname(HERE), "include")]
 DEVICE = ["-x", "hip", "--offload-arch=gfx950",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -30,7 +34,7 @@ def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OUT_DIR, src + ".o")
     cmd = [HIPCC] + COMMON
     if src.endswith(".hip"):
-        cmd += DEVICE
+        cmd += DEVICE + PER_FILE.get(src, [])
     cmd += ["-c", path, "-o", obj]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)

@@ -99,6 +99,209 @@ comet_status_t launched(hipError_t e, const char* what) {
   return ok();
 }
 
+comet_status_t gemm_common(const uint8_t* A, const uint8_t* prec, const uint16_t* sa,
+                                  const uint8_t* W, const uint16_t* sw, void* out, int M, int N,
+                                  int K, int G, comet::BlockMap* map) {
+  if (!A || !sa || !W || !sw || !out) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (M < 1 || N < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d, N=%d must be >= 1", M, N);
+  if (N % 16) return fail(COMET_ERR_INVALID_ARG, "N=%d must be a multiple of 16", N);
+  comet_status_t st = check_kg(K, G);
+  if (st) return st;
+  if (!aligned16(A) || !aligned16(sa) || !aligned16(W) || !aligned16(sw) || !aligned16(out))
+    return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  return make_map(prec, K / G, map);
+}
+
+// ---- plans and workspaces -------------------------------------------------
+
+struct PlanKey {
+  int dev, M, N, K, cus;
+  std::string mode;
+  comet::BlockMap map;
+  bool operator<(const PlanKey& o) const {
+    if (std::tie(dev, M, N, K, cus, mode) != std::tie(o.dev, o.M, o.N, o.K, o.cus, o.mode))
+      return std::tie(dev, M, N, K, cus, mode) < std::tie(o.dev, o.M, o.N, o.K, o.cus, o.mode);
+    return std::memcmp(map.bits, o.map.bits, sizeof map.bits) < 0;
+  }
+};
+
+struct DevicePlan {
+  comet::Plan host;
+  void* dmem = nullptr;  // units | wg_begin | order | split_index, one allocation
+  const comet::WorkUnit* units = nullptr;
+  const int* wg_begin = nullptr;
+  const int* order = nullptr;
+  const int* split_index = nullptr;
+};
+
+struct Workspace {
+  float* partials = nullptr;
+  size_t partial_slots = 0;
+  int* counters = nullptr;
+};
+
+std::map<PlanKey, DevicePlan> g_plans;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+std::map<int, bool> g_attr_set;
+
+std::string sched_mode() {
+  const char* m = std::getenv("COMET_SCHED");
+  return (m && *m) ? std::string(m) : std::string("cost");
+}
+
+comet::PlanOptions plan_options(int cus, const std::string& mode) {
+  comet::PlanOptions opt;
+  opt.num_cus = cus;
+  opt.tile_m = comet::kTileM;
+  opt.tile_n = comet::kTileN;
+  opt.mode = mode;
+  return opt;
+}
+
+// Plan for (device, shape, map, mode), built and uploaded on first use.
+// Caller holds g_mu.
+comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* prec,
+                        const comet::BlockMap& map, const std::string& mode, hipStream_t stream,
+                        const DevicePlan** out) {
+  PlanKey key{dev, M, N, K, cus, mode, map};
+  auto it = g_plans.find(key);
+  if (it != g_plans.end()) {
+    *out = &it->second;
+    return COMET_OK;
+  }
+  DevicePlan dp;
+  std::string err;
+  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(cus, mode), &dp.host, &err))
+    return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
+  const comet::Plan& h = dp.host;
+  std::vector<int> blob;
+  for (const comet::PlanUnit& u : h.units) {
+    blob.push_back(u.tile);
+    blob.push_back(u.g_begin);
+    blob.push_back(u.g_end);
+    blob.push_back(u.slot);
+    blob.push_back(u.nslots);
+  }
+  const size_t o_wgb = blob.size();
+  blob.insert(blob.end(), h.wg_begin.begin(), h.wg_begin.end());
+  // K-block schedule as the kernel reads it: block index, precision bit and
+  // the block's offset in A_packed (in units of M*64 bytes)
+  const size_t o_order = blob.size();
+  {
+    std::vector<int> n8_before(h.order.size() + 1, 0);
+    for (size_t g = 0; g < h.order.size(); ++g) n8_before[g + 1] = n8_before[g] + (prec[g] == 8);
+    for (int g : h.order) blob.push_back(g | (prec[g] == 8) << 10 | (g + n8_before[g]) << 11);
+  }
+  const size_t o_split = blob.size();
+  blob.insert(blob.end(), h.split_base.begin(), h.split_base.end());
+  if (std::getenv("COMET_TEST_FAIL_ALLOC")) return fail(COMET_ERR_OOM, "plan allocation failed (forced)");
+  hipError_t e = hipMalloc(&dp.dmem, blob.size() * sizeof(int));
+  if (e != hipSuccess) return fail(COMET_ERR_OOM, "plan allocation: %s", hipGetErrorString(e));
+  e = hipMemcpyAsync(dp.dmem, blob.data(), blob.size() * sizeof(int), hipMemcpyHostToDevice,
+                     stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    (void)hipFree(dp.dmem);
+    return fail(COMET_ERR_HIP, "plan upload: %s", hipGetErrorString(e));
+  }
+  int* d = static_cast<int*>(dp.dmem);
+  dp.units = reinterpret_cast<const comet::WorkUnit*>(d);
+  dp.wg_begin = d + o_wgb;
+  dp.order = d + o_order;
+  dp.split_index = d + o_split;
+  if (std::getenv("COMET_LOG"))
+    std::fprintf(stderr,
+                 "[comet] plan M=%d N=%d K=%d mode=%s tiles=%dx%d wgs=%d units=%zu split_tiles=%d "
+                 "partial_slots=%d cost max/mean=%.3f\n",
+                 M, N, K, mode.c_str(), h.tiles_m, h.tiles_n, h.num_wgs, h.units.size(),
+                 h.split_tiles, h.partial_slots, h.mean_wg_cost > 0 ? h.max_wg_cost / h.mean_wg_cost : 0.0);
+  *out = &g_plans.emplace(key, std::move(dp)).first->second;
+  return COMET_OK;
+}
+
+// Split-tile workspace of (device, stream), grown to `slots` partial tiles.
+// Caller holds g_mu.
+comet_status_t get_workspace(int dev, hipStream_t stream, size_t slots, Workspace** out) {
+  Workspace& ws = g_ws[{dev, stream}];
+  if (slots > ws.partial_slots) {
+    if (ws.partials) {
+      // the previous launch on this stream may still use them
+      hipError_t e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) return fail(COMET_ERR_HIP, "workspace sync: %s", hipGetErrorString(e));
+      (void)hipFree(ws.partials);
+      (void)hipFree(ws.counters);
+      ws = Workspace{};
+    }
+    const size_t tile = (size_t)comet::kTileM * comet::kTileN * sizeof(float);
+    hipError_t e = hipMalloc(&ws.partials, slots * tile);
+    if (e != hipSuccess) {
+      ws = Workspace{};
+      return fail(COMET_ERR_OOM, "workspace allocation: %s", hipGetErrorString(e));
+    }
+    e = hipMalloc(&ws.counters, slots * sizeof(int));
+    if (e == hipSuccess) e = hipMemsetAsync(ws.counters, 0, slots * sizeof(int), stream);
+    if (e != hipSuccess) {
+      (void)hipFree(ws.partials);
+      ws = Workspace{};
+      return fail(COMET_ERR_OOM, "workspace counters: %s", hipGetErrorString(e));
+    }
+    ws.partial_slots = slots;
+  }
+  *out = &ws;
+  return COMET_OK;
+}
+
+comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* sa,
+                        const uint8_t* W, const uint16_t* sw, uint16_t* out, int32_t* acc, int M,
+                        int N, int K, const comet::BlockMap& map, int m0, int m1, int n0, int n1,
+                        hipStream_t stream) {
+  int dev;
+  DeviceInfo info;
+  comet_status_t st = current_device(&dev, &info);
+  if (st) return st;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_attr_set[dev]) {
+    hipError_t e = comet::set_gemm_attributes();
+    if (e != hipSuccess) return fail(COMET_ERR_HIP, "kernel attributes: %s", hipGetErrorString(e));
+    g_attr_set[dev] = true;
+  }
+  const bool diag = acc != nullptr;
+  const DevicePlan* plan;
+  // the diagnostic form always runs whole tiles (no split partials)
+  if ((st = get_plan(dev, info.cus, M, N, K, prec, map, diag ? std::string("dp") : sched_mode(),
+                     stream, &plan)))
+    return st;
+  Workspace* ws = nullptr;
+  if (plan->host.partial_slots > 0 &&
+      (st = get_workspace(dev, stream, (size_t)plan->host.partial_slots, &ws)))
+    return st;
+  comet::GemmArgs a{};
+  a.A = A;
+  a.sa = sa;
+  a.W = W;
+  a.sw = sw;
+  a.out = out;
+  a.acc = acc;
+  a.partials = ws ? ws->partials : nullptr;
+  a.counters = ws ? ws->counters : nullptr;
+  a.units = plan->units;
+  a.wg_begin = plan->wg_begin;
+  a.order = plan->order;
+  a.split_index = plan->split_index;
+  a.n4 = 0;
+  for (int g = 0; g < K / comet::kG; ++g) a.n4 += prec[g] == 4;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.tiles_n = plan->host.tiles_n;
+  a.win_m0 = m0;
+  a.win_m1 = m1;
+  a.win_n0 = n0;
+  a.win_n1 = n1;
+  a.map = map;
+  return launched(comet::launch_gemm(a, plan->host.num_wgs, diag, stream), "gemm launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -158,19 +361,6 @@ comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_s
   return launched(comet::launch_pack_w4(W, W_packed, w_scales, N, K, stream), "pack_w4 launch");
 }
 
-static comet_status_t gemm_common(const uint8_t* A, const uint8_t* prec, const uint16_t* sa,
-                                  const uint8_t* W, const uint16_t* sw, void* out, int M, int N,
-                                  int K, int G, comet::BlockMap* map) {
-  if (!A || !sa || !W || !sw || !out) return fail(COMET_ERR_INVALID_ARG, "null pointer");
-  if (M < 1 || N < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d, N=%d must be >= 1", M, N);
-  if (N % 16) return fail(COMET_ERR_INVALID_ARG, "N=%d must be a multiple of 16", N);
-  comet_status_t st = check_kg(K, G);
-  if (st) return st;
-  if (!aligned16(A) || !aligned16(sa) || !aligned16(W) || !aligned16(sw) || !aligned16(out))
-    return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
-  return make_map(prec, K / G, map);
-}
-
 comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* prec,
                                const uint16_t* a_scales, const uint8_t* W_packed,
                                const uint16_t* w_scales, uint16_t* out, int M, int N, int K,
@@ -179,21 +369,8 @@ comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* prec,
   comet_status_t st =
       gemm_common(A_packed, prec, a_scales, W_packed, w_scales, out, M, N, K, G, &map);
   if (st) return st;
-  int dev;
-  DeviceInfo info;
-  if ((st = current_device(&dev, &info))) return st;
-  comet::GemmArgs a{};
-  a.A = A_packed;
-  a.sa = a_scales;
-  a.W = W_packed;
-  a.sw = w_scales;
-  a.out = out;
-  a.M = M;
-  a.N = N;
-  a.K = K;
-  a.tiles_n = (N + comet::kTileN - 1) / comet::kTileN;
-  a.map = map;
-  return launched(comet::launch_gemm_simple(a, false, stream), "gemm launch");
+  return run_gemm(A_packed, prec, a_scales, W_packed, w_scales, out, nullptr, M, N, K, map, 0, 0,
+                  0, 0, stream);
 }
 
 comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* prec,
@@ -207,25 +384,8 @@ comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* prec,
   if (m0 < 0 || m1 > M || m0 >= m1 || n0 < 0 || n1 > N || n0 >= n1)
     return fail(COMET_ERR_INVALID_ARG, "window [%d,%d)x[%d,%d) is empty or outside %dx%d", m0,
                 m1, n0, n1, M, N);
-  int dev;
-  DeviceInfo info;
-  if ((st = current_device(&dev, &info))) return st;
-  comet::GemmArgs a{};
-  a.A = A_packed;
-  a.sa = a_scales;
-  a.W = W_packed;
-  a.sw = w_scales;
-  a.acc = acc;
-  a.M = M;
-  a.N = N;
-  a.K = K;
-  a.tiles_n = (N + comet::kTileN - 1) / comet::kTileN;
-  a.win_m0 = m0;
-  a.win_m1 = m1;
-  a.win_n0 = n0;
-  a.win_n1 = n1;
-  a.map = map;
-  return launched(comet::launch_gemm_simple(a, true, stream), "gemm_acc launch");
+  return run_gemm(A_packed, prec, a_scales, W_packed, w_scales, nullptr, acc, M, N, K, map, m0, m1,
+                  n0, n1, stream);
 }
 
 comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* prec, int num_cus,
@@ -276,6 +436,21 @@ comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* p
 
 void comet_release_caches(void) {
   std::lock_guard<std::mutex> lk(g_mu);
+  int cur = -1;
+  (void)hipGetDevice(&cur);
+  for (auto& kv : g_plans) {
+    (void)hipSetDevice(kv.first.dev);
+    (void)hipFree(kv.second.dmem);
+  }
+  for (auto& kv : g_ws) {
+    (void)hipSetDevice(kv.first.first);
+    (void)hipFree(kv.second.partials);
+    (void)hipFree(kv.second.counters);
+  }
+  if (cur >= 0) (void)hipSetDevice(cur);
+  g_plans.clear();
+  g_ws.clear();
+  g_attr_set.clear();
   g_devices.clear();
 }
 

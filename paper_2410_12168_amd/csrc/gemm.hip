@@ -9,8 +9,27 @@
 // W4A8.  Products of such codes are integers times 2^-18 and their sums stay
 // below 2^24 units, so the fp32 MFMA result is the exact block sum (the
 // paper's integer tile result, Sec. 4.1) and needs no int->float convert.
-// Dequantization (Sec. 4.3, scale divided by the zero-extension factor):
-//     C += Y * (sa * 2^18) * sw      in fp32, once per output and K-block.
+// Dequantization (Sec. 4.3: the scale absorbs the conversion factor):
+//     C += Y * P,  P = (sa * 2^18) * sw      in fp32, once per output and K-block.
+// The scale products P of a 16x16 block are one v_mfma_f32_4x4x1_16b_f32
+// (16 outer products of 4 activation scales and 4 weight scales, K = 1, exact
+// in fp32), laid out lane for lane like Y, so the vector ALUs only do the
+// fused multiply-add; they are the co-bottleneck of this kernel.
+//
+// Kernel structure (the gfx950 form of the paper's software pipeline,
+// Sec. 4.2, and of its tile decomposition, Sec. 4.4):
+//   * persistent workgroups of 8 waves walk a host-built list of work units
+//     (tile, K-block range); full tiles go to one workgroup, the fractional
+//     last wave of tiles is split over all of them by cost;
+//   * per K-block the workgroup stages its 256x256 tile's operands
+//     HBM -> VGPR (128-bit loads) -> unpack -> LDS (double-buffered, XOR
+//     swizzled rows), so every nibble is unpacked once per workgroup, and one
+//     barrier per K-block separates the stages;
+//   * each wave computes a 128x64 quadrant: 8x4 MFMA blocks per K-block, fed
+//     from LDS, with the fp32 dequantization interleaved;
+//   * split tiles write fp32 partials; the last workgroup to finish a tile
+//     (arrival counter, no waiting) adds the partials in slot order and
+//     stores fp16, so the result does not depend on arrival order.
 #include <hip/hip_runtime.h>
 #include <hip/hip_fp16.h>
 #include <stdint.h>
@@ -23,158 +42,378 @@ namespace {
 
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kSignMag = 0x87878787u;
 constexpr float kUnit = 262144.0f;  // 2^18: (2^-9)^2 of the FP8 code encoding
 
-__device__ inline uint32_t rotr4(uint32_t w) { return __builtin_amdgcn_alignbit(w, w, 4); }
+constexpr int kThreads = 512;            // 8 waves
+constexpr int kWM = 128, kWN = 64;       // wave quadrant
+constexpr int kRB = kWM / 16, kCB = kWN / 16;
+constexpr int kA = kTileM * 128;         // LDS bytes of one A stage (fp8 or raw 8-bit codes)
+constexpr int kW = kTileN * 128;         // LDS bytes of one W stage (fp8)
+constexpr int kBuf = kA + kW + 4 * kTileM + 4 * kTileN;
+constexpr int kLds = 2 * kBuf;
 
-// 16 bytes of 4-bit codes (32 channels) -> 8 dwords of FP8 operand bytes.
-__device__ inline i32x8 unpack4(uint4 v) {
-  i32x8 r;
-  r[0] = (int)(v.x & kSignMag);
-  r[1] = (int)(rotr4(v.x) & kSignMag);
-  r[2] = (int)(v.y & kSignMag);
-  r[3] = (int)(rotr4(v.y) & kSignMag);
-  r[4] = (int)(v.z & kSignMag);
-  r[5] = (int)(rotr4(v.z) & kSignMag);
-  r[6] = (int)(v.w & kSignMag);
-  r[7] = (int)(rotr4(v.w) & kSignMag);
-  return r;
+static_assert(kTileM == 2 * kWM && kTileN == 4 * kWN, "8 waves as 2 x 4 quadrants");
+
+__device__ __forceinline__ uint32_t rotr4(uint32_t w) { return __builtin_amdgcn_alignbit(w, w, 4); }
+
+// 16 bytes of 4-bit codes (32 channels) -> 32 FP8 bytes, natural channel order.
+__device__ __forceinline__ void unpack4(u32x4 v, u32x4& lo, u32x4& hi) {
+  lo = u32x4{v[0] & kSignMag, rotr4(v[0]) & kSignMag, v[1] & kSignMag, rotr4(v[1]) & kSignMag};
+  hi = u32x4{v[2] & kSignMag, rotr4(v[2]) & kSignMag, v[3] & kSignMag, rotr4(v[3]) & kSignMag};
 }
 
-// 32 bytes of 8-bit codes -> hi (|code| >> 3 with sign) and lo (|code| & 7 with sign).
-__device__ inline void unpack8(uint4 a, uint4 b, i32x8& hi, i32x8& lo) {
-  uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-  #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    lo[i] = (int)(w[i] & kSignMag);
-    hi[i] = (int)(((w[i] >> 3) & 0x0F0F0F0Fu) | (w[i] & 0x80808080u));
-  }
-}
+// 8-bit codes -> FP8 of the high part (|code| >> 3, signed) and low part (|code| & 7, signed).
+__device__ __forceinline__ uint32_t hi8(uint32_t w) { return ((w >> 3) & 0x0F0F0F0Fu) | (w & 0x80808080u); }
+__device__ __forceinline__ uint32_t lo8(uint32_t w) { return w & kSignMag; }
 
-__device__ inline f32x4 mfma_fp8(i32x8 a, i32x8 b, f32x4 c) {
+__device__ __forceinline__ f32x4 mfma_fp8(const i32x8& a, const i32x8& b, f32x4 c) {
   // cbsz = blgp = 0: both operands OCP FP8-E4M3; zero scale operands select
   // the unscaled instruction.
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-__device__ inline float h2f(uint16_t h) { return __half2float(__ushort_as_half(h)); }
+// LDS layout of one stage buffer: A (kTileM rows x 128 B), W (kTileN rows x
+// 128 B), then the tile's fp32 activation scales (times 2^18) and weight
+// scales.  Row r's 16-byte chunk c sits at r*128 + ((c ^ (r & 7)) << 4): the
+// XOR swizzle spreads the 16 rows of one MFMA operand fetch over all banks.
+__device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 
-// Data-parallel kernel: one 128x128 output tile per workgroup of 4 waves, each
-// wave a 64x64 quadrant (4x4 blocks of 16x16).  Operands are read straight
-// from global memory into registers.  All loads clamp their row/column into
-// range, so edge tiles never read out of bounds; stores are masked.
-template <bool DIAG>
-__global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int r16 = lane & 15;
-  const int q4 = lane >> 4;
-  const int tile = blockIdx.x;
-  const int tm = tile / a.tiles_n;
-  const int tn = tile % a.tiles_n;
-  const int row0 = tm * kTileM + (wave >> 1) * 64;
-  const int col0 = tn * kTileN + (wave & 1) * 64;
-  const int M = a.M, N = a.N, K = a.K;
-  const int NG = K / kG;
-  const size_t wrow = (size_t)(K / 2);
+__device__ __forceinline__ i32x8 lds_frag(const uint8_t* p0, const uint8_t* p1) {
+  const u32x4 x = *reinterpret_cast<const u32x4*>(p0);
+  const u32x4 y = *reinterpret_cast<const u32x4*>(p1);
+  i32x8 f;
+  f[0] = (int)x[0]; f[1] = (int)x[1]; f[2] = (int)x[2]; f[3] = (int)x[3];
+  f[4] = (int)y[0]; f[5] = (int)y[1]; f[6] = (int)y[2]; f[7] = (int)y[3];
+  return f;
+}
 
-  f32x4 C[4][4];
+// Per-lane LDS offsets, fixed for the whole kernel.  Fragment reads of row
+// block rb (column block cb) add rb*2048 (cb*2048): 16 rows of 128 bytes, and
+// the swizzle term depends only on the row's low 3 bits, which do not change.
+struct LaneOffsets {
+  int fa0, fa1;   // A fragment chunks (2*q4, 2*q4+1) of row wr + r16
+  int fw0, fw1;   // W fragment chunks of row wc + r16
+  int st4a, st4b; // staging stores, 4-bit path: chunks (2*part, 2*part+1) of row tid/4
+  int st8;        // staging store, 8-bit activations: chunk tid%8 of row tid/8
+};
+
+__device__ __forceinline__ LaneOffsets lane_offsets() {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const int wr = (wave >> 2) * kWM, wc = (wave & 3) * kWN;
+  LaneOffsets o;
+  o.fa0 = swz(wr + r16, 2 * q4);
+  o.fa1 = swz(wr + r16, 2 * q4 + 1);
+  o.fw0 = kA + swz(wc + r16, 2 * q4);
+  o.fw1 = kA + swz(wc + r16, 2 * q4 + 1);
+  o.st4a = swz(tid >> 2, 2 * (tid & 3));
+  o.st4b = swz(tid >> 2, 2 * (tid & 3) + 1);
+  o.st8 = swz(tid >> 3, tid & 7);
+  return o;
+}
+
+// Per-lane global offsets of one output tile (rows and columns clamped into
+// range, so edge tiles never read out of bounds; clamped rows and columns
+// compute values that are never stored).
+struct TileOffsets {
+  uint32_t a4[2];  // A_packed 4-bit block: row (tid/4 + 128 i) * 64 + (tid%4) * 16
+  uint32_t a8[4];  // A_packed 8-bit block: row (tid/8 + 64 i) * 128 + (tid%8) * 16
+  uint32_t w[2];   // W_packed: col (tid/4 + 128 i) * K/2 + (tid%4) * 16
+  uint32_t s;      // scale index: row (tid < 256) or column (tid >= 256)
+};
+
+__device__ __forceinline__ TileOffsets tile_offsets(const GemmArgs& p, int m0, int n0) {
+  const int tid = threadIdx.x;
+  TileOffsets t;
+  #pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    t.a4[i] = (uint32_t)min(m0 + (tid >> 2) + 128 * i, p.M - 1) * 64u + (tid & 3) * 16u;
+    t.w[i] = (uint32_t)min(n0 + (tid >> 2) + 128 * i, p.N - 1) * (uint32_t)(p.K / 2) +
+             (tid & 3) * 16u;
+  }
   #pragma unroll
   for (int i = 0; i < 4; ++i)
-    #pragma unroll
-    for (int j = 0; j < 4; ++j) C[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    t.a8[i] = (uint32_t)min(m0 + (tid >> 3) + 64 * i, p.M - 1) * 128u + (tid & 7) * 16u;
+  t.s = tid < kTileM ? (uint32_t)min(m0 + tid, p.M - 1) : (uint32_t)min(n0 + tid - kTileM, p.N - 1);
+  return t;
+}
 
-  int n8 = 0;  // 8-bit blocks before g (for the block-major A offset)
-  for (int g = 0; g < NG; ++g) {
-    const bool b8 = (a.map.bits[g >> 6] >> (g & 63)) & 1;
-    const size_t abase = (size_t)M * 64 * (size_t)(g + n8);
-    n8 += b8 ? 1 : 0;
+// One K-block position of the schedule, decoded from the host's encoding:
+// bits 0..9 block index g, bit 10 set for an 8-bit activation block, bits
+// 11.. the block's offset in A_packed in units of M*64 bytes.
+struct KBlock {
+  int g;
+  bool b8;
+  int aoff;
+};
 
-    i32x8 wf[4];
-    float swf[4];
-    #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      const int col = min(col0 + cb * 16 + r16, N - 1);
-      uint4 v = *reinterpret_cast<const uint4*>(a.W + (size_t)col * wrow + (size_t)g * 64 + q4 * 16);
-      wf[cb] = unpack4(v);
-      swf[cb] = h2f(a.sw[(size_t)g * N + col]);
-    }
-    float saf[4][4];
-    #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-      #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = min(row0 + rb * 16 + 4 * q4 + i, M - 1);
-        saf[rb][i] = h2f(a.sa[(size_t)g * M + row]) * kUnit;
-      }
+__device__ __forceinline__ KBlock kblock(int e) { return KBlock{e & 1023, ((e >> 10) & 1) != 0, e >> 11}; }
 
-    #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-      const int arow = min(row0 + rb * 16 + r16, M - 1);
-      i32x8 af, ahi;
-      if (b8) {
-        const uint8_t* p = a.A + abase + (size_t)arow * 128 + q4 * 32;
-        uint4 v0 = *reinterpret_cast<const uint4*>(p);
-        uint4 v1 = *reinterpret_cast<const uint4*>(p + 16);
-        unpack8(v0, v1, ahi, af);
-      } else {
-        uint4 v = *reinterpret_cast<const uint4*>(a.A + abase + (size_t)arow * 64 + q4 * 16);
-        af = unpack4(v);
-      }
-      #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        f32x4 y = mfma_fp8(af, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
-        if (b8) {
-          f32x4 yh = mfma_fp8(ahi, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
-          #pragma unroll
-          for (int i = 0; i < 4; ++i) y[i] = __builtin_fmaf(yh[i], 8.0f, y[i]);  // exact
-        }
-        if (DIAG) {
-          const int col = col0 + cb * 16 + r16;
-          #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int row = row0 + rb * 16 + 4 * q4 + i;
-            if (row >= a.win_m0 && row < a.win_m1 && col >= a.win_n0 && col < a.win_n1) {
-              const size_t idx = ((size_t)(row - a.win_m0) * (a.win_n1 - a.win_n0) +
-                                  (col - a.win_n0)) * NG + g;
-              a.acc[idx] = (int32_t)(y[i] * kUnit);
-            }
-          }
-        } else {
-          #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            C[rb][cb][i] = __builtin_fmaf(y[i], saf[rb][i] * swf[cb], C[rb][cb][i]);
-        }
-      }
-    }
-  }
-  if (DIAG) return;
+// Registers holding one K-block's packed operands between load and LDS store.
+struct Stage {
+  u32x4 a[4];
+  u32x4 w[2];
+  uint32_t s;
+};
+
+__device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, const TileOffsets& t,
+                                  Stage& st) {
+  const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)kb.aoff;
+  // two loads per lane for a 4-bit block, four for an 8-bit one; the first
+  // two only switch offsets (a select, not a branch, keeps st in registers)
+  const uint32_t sel = 0u - (uint32_t)kb.b8;
   #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t off = t.a4[i] ^ ((t.a4[i] ^ t.a8[i]) & sel);
+    st.a[i] = *reinterpret_cast<const u32x4*>(A + off);
+  }
+  if (kb.b8) {
     #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      const int col = col0 + cb * 16 + r16;
+    for (int i = 2; i < 4; ++i) st.a[i] = *reinterpret_cast<const u32x4*>(A + t.a8[i]);
+  }
+  const uint8_t* W = p.W + (size_t)kb.g * 64;
+  #pragma unroll
+  for (int i = 0; i < 2; ++i) st.w[i] = *reinterpret_cast<const u32x4*>(W + t.w[i]);
+  if (threadIdx.x < kTileM)
+    st.s = p.sa[(size_t)kb.g * p.M + t.s];
+  else
+    st.s = p.sw[(size_t)kb.g * p.N + t.s];
+}
+
+__device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* buf, const LaneOffsets& o) {
+  const int tid = threadIdx.x;
+  if (!b8) {
+    #pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      u32x4 lo, hi;
+      unpack4(st.a[i], lo, hi);
+      *reinterpret_cast<u32x4*>(buf + o.st4a + i * 16384) = lo;
+      *reinterpret_cast<u32x4*>(buf + o.st4b + i * 16384) = hi;
+    }
+  } else {
+    #pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + o.st8 + i * 8192) = st.a[i];
+  }
+  #pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    u32x4 lo, hi;
+    unpack4(st.w[i], lo, hi);
+    *reinterpret_cast<u32x4*>(buf + kA + o.st4a + i * 16384) = lo;
+    *reinterpret_cast<u32x4*>(buf + kA + o.st4b + i * 16384) = hi;
+  }
+  // Scales, permuted so that each lane later reads its values with one or two
+  // 16-byte LDS reads.  Activation scale of tile row r = 128h + 16rb + 4j + i
+  // goes to (16h + 4j + i) * 8 + rb (the 8 row blocks of one 4x4x1 operand
+  // lane); weight scale of tile column c = 64q + 16cb + x to
+  // kTileM + (16q + x) * 4 + cb.
+  const float f = __half2float(__ushort_as_half((unsigned short)st.s));
+  float* scales = reinterpret_cast<float*>(buf + kA + kW);
+  if (tid < kTileM) {
+    const int r = tid, h = r >> 7, rb = (r >> 4) & 7, j = (r >> 2) & 3, i = r & 3;
+    scales[(16 * h + 4 * j + i) * 8 + rb] = f * kUnit;
+  } else {
+    const int c = tid - kTileM, q = c >> 6, cb = (c >> 4) & 3, x = c & 15;
+    scales[kTileM + (16 * q + x) * 4 + cb] = f;
+  }
+}
+
+__device__ __forceinline__ f32x4 scale_products(float sa, float sw) {
+  // lane l receives sa(lane 4*(l/4) + i) * sw(lane l) for i = 0..3, which with
+  // the operand lanes chosen in compute_block is the 16x16 accumulator layout
+  return __builtin_amdgcn_mfma_f32_4x4x1f32(sa, sw, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+}
+
+template <bool DIAG, bool B8>
+__device__ __forceinline__ void compute_block(const uint8_t* buf, const LaneOffsets& o, int g, int NG,
+                                              int m0, int n0, const GemmArgs& p,
+                                              f32x4 (&C)[kRB][kCB]) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const int wr = (wave >> 2) * kWM;
+  const int wc = (wave & 3) * kWN;
+  // this lane's 4x4x1 operands: activation scale of row wr + 16rb + 4*q4 + (lane & 3)
+  // for every rb, weight scale of column wc + 16cb + r16 for every cb
+  const float* scales = reinterpret_cast<const float*>(buf + kA + kW);
+  const f32x4 sal0 = *reinterpret_cast<const f32x4*>(scales + (16 * (wave >> 2) + 4 * q4 + (lane & 3)) * 8);
+  const f32x4 sal1 = *reinterpret_cast<const f32x4*>(scales + (16 * (wave >> 2) + 4 * q4 + (lane & 3)) * 8 + 4);
+  const f32x4 swl = *reinterpret_cast<const f32x4*>(scales + kTileM + (16 * (wave & 3) + r16) * 4);
+
+  i32x8 wf[kCB];
+  #pragma unroll
+  for (int cb = 0; cb < kCB; ++cb) wf[cb] = lds_frag(buf + o.fw0 + cb * 2048, buf + o.fw1 + cb * 2048);
+  #pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) {
+    i32x8 af = lds_frag(buf + o.fa0 + rb * 2048, buf + o.fa1 + rb * 2048);
+    const float sa_rb = rb < 4 ? sal0[rb & 3] : sal1[rb & 3];
+    i32x8 ah;
+    if constexpr (B8) {
       #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = row0 + rb * 16 + 4 * q4 + i;
-        if (row < M && col < N)
-          a.out[(size_t)row * N + col] = __half_as_ushort(__float2half_rn(C[rb][cb][i]));
+      for (int i = 0; i < 8; ++i) {
+        ah[i] = (int)hi8((uint32_t)af[i]);
+        af[i] = (int)lo8((uint32_t)af[i]);
       }
     }
+    #pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) {
+      f32x4 y = mfma_fp8(af, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
+      if constexpr (B8) {
+        const f32x4 yh = mfma_fp8(ah, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) y[i] = __builtin_fmaf(yh[i], 8.0f, y[i]);  // exact
+      }
+      if constexpr (DIAG) {
+        const int col = n0 + wc + cb * 16 + r16;
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = m0 + wr + rb * 16 + 4 * q4 + i;
+          if (row >= p.win_m0 && row < p.win_m1 && col >= p.win_n0 && col < p.win_n1) {
+            const size_t idx = ((size_t)(row - p.win_m0) * (p.win_n1 - p.win_n0) +
+                                (col - p.win_n0)) * NG + g;
+            p.acc[idx] = (int32_t)(y[i] * kUnit);
+          }
+        }
+      } else {
+        const f32x4 P = scale_products(sa_rb, swl[cb]);
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) C[rb][cb][i] = __builtin_fmaf(y[i], P[i], C[rb][cb][i]);
+      }
+    }
+    // Pin this row block's accumulator updates here.  Without it the
+    // optimizer sinks the FMAs past the barrier into the next K-block, keeping
+    // all 32 MFMA results of the K-block live at once (and spilling them).
+    if constexpr (!DIAG)
+      asm volatile("" : "+v"(C[rb][0]), "+v"(C[rb][1]), "+v"(C[rb][2]), "+v"(C[rb][3]));
+  }
+}
+
+// Pipelined K-loop over schedule positions [pos, end), all of precision B8:
+// K-block k is computed from one LDS buffer while k+1 (whatever its
+// precision) is loaded into registers and then stored to the other buffer.
+template <bool DIAG, bool B8>
+__device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o,
+                                      const TileOffsets& t, uint8_t* smem, int g_begin, int pos,
+                                      int end, int g_end, int NG, int m0, int n0, Stage& st,
+                                      f32x4 (&C)[kRB][kCB]) {
+  for (; pos < end; ++pos) {
+    const int cur = (pos - g_begin) & 1;
+    const bool more = pos + 1 < g_end;
+    const KBlock kb = kblock(p.order[pos]);
+    const KBlock kn = kblock(p.order[more ? pos + 1 : pos]);
+    if (more) stage_load(p, kn, t, st);
+    compute_block<DIAG, B8>(smem + cur * kBuf, o, kb.g, NG, m0, n0, p, C);
+    if (more) stage_store(st, kn.b8, smem + (cur ^ 1) * kBuf, o);
+    __syncthreads();
+  }
+}
+
+template <bool DIAG>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  __shared__ int s_last;
+  const int NG = p.K / kG;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const LaneOffsets o = lane_offsets();
+  const int u_end = p.wg_begin[blockIdx.x + 1];
+
+  for (int u = p.wg_begin[blockIdx.x]; u < u_end; ++u) {
+    const WorkUnit unit = p.units[u];
+    const int tm = unit.tile / p.tiles_n, tn = unit.tile % p.tiles_n;
+    const int m0 = tm * kTileM, n0 = tn * kTileN;
+    const TileOffsets t = tile_offsets(p, m0, n0);
+
+    f32x4 C[kRB][kCB];
+    #pragma unroll
+    for (int i = 0; i < kRB; ++i)
+      #pragma unroll
+      for (int j = 0; j < kCB; ++j) C[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // software pipeline over the unit's K-blocks; the schedule lists all
+    // 4-bit blocks before the 8-bit ones, so each precision runs its own loop
+    Stage st;
+    const KBlock k0 = kblock(p.order[unit.g_begin]);
+    stage_load(p, k0, t, st);
+    stage_store(st, k0.b8, smem, o);
+    __syncthreads();
+    const int split = min(max(p.n4, unit.g_begin), unit.g_end);
+    kloop<DIAG, false>(p, o, t, smem, unit.g_begin, unit.g_begin, split, unit.g_end, NG, m0, n0,
+                       st, C);
+    kloop<DIAG, true>(p, o, t, smem, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0, n0, st,
+                      C);
+    if (DIAG) continue;
+
+    const int wr = (wave >> 2) * kWM, wc = (wave & 3) * kWN;
+    if (unit.nslots > 1) {
+      // split tile: publish this slot's partial, then the last arriver reduces
+      const int base = p.split_index[unit.tile];
+      float* part = p.partials + (size_t)(base + unit.slot) * (kTileM * kTileN);
+      #pragma unroll
+      for (int rb = 0; rb < kRB; ++rb)
+        #pragma unroll
+        for (int cb = 0; cb < kCB; ++cb)
+          *reinterpret_cast<f32x4*>(part + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4) =
+              C[rb][cb];
+      __threadfence();
+      __syncthreads();
+      if (threadIdx.x == 0) s_last = atomicAdd(p.counters + base, 1) == unit.nslots - 1;
+      __syncthreads();
+      if (!s_last) continue;
+      __threadfence();
+      #pragma unroll
+      for (int rb = 0; rb < kRB; ++rb)
+        #pragma unroll
+        for (int cb = 0; cb < kCB; ++cb) C[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < unit.nslots; ++s) {
+        const float* src = p.partials + (size_t)(base + s) * (kTileM * kTileN);
+        #pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) {
+          #pragma unroll
+          for (int cb = 0; cb < kCB; ++cb)
+            C[rb][cb] += *reinterpret_cast<const f32x4*>(
+                src + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      if (threadIdx.x == 0) p.counters[base] = 0;  // ready for the next launch
+    }
+    #pragma unroll
+    for (int rb = 0; rb < kRB; ++rb)
+      #pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) {
+        const int col = n0 + wc + cb * 16 + r16;
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = m0 + wr + rb * 16 + 4 * q4 + i;
+          if (row < p.M && col < p.N)
+            p.out[(size_t)row * p.N + col] = __half_as_ushort(__float2half_rn(C[rb][cb][i]));
+        }
+      }
+  }
 }
 
 }  // namespace
 
-hipError_t launch_gemm_simple(const GemmArgs& a, bool diag, hipStream_t stream) {
-  const int tiles_m = (a.M + kTileM - 1) / kTileM;
-  const int tiles = tiles_m * a.tiles_n;
+int gemm_lds_bytes() { return kLds; }
+
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, hipStream_t stream) {
   if (diag)
-    hipLaunchKernelGGL(gemm_simple_kernel<true>, dim3(tiles), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(gemm_kernel<true>, dim3(num_wgs), dim3(kThreads), kLds, stream, a);
   else
-    hipLaunchKernelGGL(gemm_simple_kernel<false>, dim3(tiles), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(gemm_kernel<false>, dim3(num_wgs), dim3(kThreads), kLds, stream, a);
   return hipGetLastError();
+}
+
+hipError_t set_gemm_attributes() {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<false>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<true>),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
 }
 
 }  // namespace comet

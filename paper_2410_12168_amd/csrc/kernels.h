@@ -37,7 +37,8 @@ struct GemmArgs {
   int* counters;      // per split tile arrival counters (zero between launches)
   const WorkUnit* units;
   const int* wg_begin;
-  const int* order;   // K-block order, K/G entries
+  const int* order;   // K-block schedule, K/G entries: g | is8 << 10 | (g + 8-bit blocks before g) << 11
+  int n4;             // number of 4-bit blocks (they come first in `order`)
   const int* split_index;  // tile -> index into the partial/counter arrays (-1: not split)
   int M, N, K;
   int tiles_n;        // tiles along N
@@ -50,10 +51,14 @@ hipError_t launch_quantize_act(const uint16_t* X, uint8_t* A, uint16_t* sa, int 
 hipError_t launch_pack_w4(const uint16_t* W, uint8_t* Wp, uint16_t* sw, int N, int K,
                           hipStream_t stream);
 
-// Output-tile edge of the GEMM kernels.
-constexpr int kTileM = 128;
-constexpr int kTileN = 128;
+// Output tile of one GEMM workgroup.
+constexpr int kTileM = 256;
+constexpr int kTileN = 256;
 
-hipError_t launch_gemm_simple(const GemmArgs& a, bool diag, hipStream_t stream);
+// Persistent GEMM: `num_wgs` workgroups walk a.units (a.wg_begin per group).
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, hipStream_t stream);
+// Allows the GEMM's dynamic LDS size; once per process and device.
+hipError_t set_gemm_attributes();
+int gemm_lds_bytes();
 
 }  // namespace comet

@@ -135,7 +135,7 @@ def test_edge_values_quantize():
     assert np.array_equal(host(A), oracle.pack_act(qa, prec))
 
 
-@pytest.mark.parametrize("layer", ["gate_up", "down"])
+@pytest.mark.parametrize("layer", ["qkv", "gate_up", "down"])
 def test_llama3_70b_full_size_sampled_rows(layer):
     # full LLaMA-3-70B prefill shape (M = 4096); the oracle recomputes a seeded
     # sample of rows (quantization is per row), the weights in full
