@@ -44,6 +44,11 @@ def parse():
     ap.add_argument("--workload", default="llama3-70b-prefill", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--frac8", type=float, default=1 / 16)
+    ap.add_argument("--layers", default="",
+                    help="comma-separated subset of the workload's layers (default: all)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run one device-to-device copy of this many MiB (a "
+                         "known-size reference for HBM byte counters)")
     ap.add_argument("--cpu-rows", type=int, default=512,
                     help="token rows per layer in the CPU-oracle sample (0: skip)")
     return ap.parse_args()
@@ -68,7 +73,10 @@ def main():
     shapes = getattr(synth, wl["layers"])
     layers = []
     t_setup = time.time()
+    wanted = [x for x in args.layers.split(",") if x] or list(shapes)
     for name, (K, N) in shapes.items():
+        if name not in wanted:
+            continue
         NG = K // 128
         n8 = int(round(NG * args.frac8))
         prec = synth.prec_map(NG, n8)
@@ -175,6 +183,13 @@ def main():
         "layers": per_layer,
         "setup_s": round(t_setup, 1),
     }
+
+    if args.copy_mib > 0:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        record["copy_mib"] = args.copy_mib
 
     if args.cpu_rows > 0:
         record["cpu_baseline"] = cpu_baseline(layers, args.cpu_rows)

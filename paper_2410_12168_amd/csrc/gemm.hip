@@ -77,9 +77,11 @@ __device__ __forceinline__ f32x4 mfma_fp8(const i32x8& a, const i32x8& b, f32x4 
 
 // LDS layout of one stage buffer: A (kTileM rows x 128 B), W (kTileN rows x
 // 128 B), then the tile's fp32 activation scales (times 2^18) and weight
-// scales.  Row r's 16-byte chunk c sits at r*128 + ((c ^ (r & 7)) << 4): the
-// XOR swizzle spreads the 16 rows of one MFMA operand fetch over all banks.
-__device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+// scales.  Row r's 16-byte chunk c sits at r*128 + ((c ^ g(r)) << 4) with
+// g(r) = (r ^ (r >> 1)) & 7.  With this swizzle the 16 rows of one MFMA
+// operand fetch (ds_read_b128) are bank-conflict free on gfx950 (measured:
+// the plain c ^ (r & 7) swizzle runs at 60% of the read bandwidth).
+__device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ ((r ^ (r >> 1)) & 7)) << 4); }
 
 __device__ __forceinline__ i32x8 lds_frag(const uint8_t* p0, const uint8_t* p1) {
   const u32x4 x = *reinterpret_cast<const u32x4*>(p0);
@@ -92,12 +94,10 @@ __device__ __forceinline__ i32x8 lds_frag(const uint8_t* p0, const uint8_t* p1) 
 
 // Per-lane LDS offsets, fixed for the whole kernel.  Fragment reads of row
 // block rb (column block cb) add rb*2048 (cb*2048): 16 rows of 128 bytes, and
-// the swizzle term depends only on the row's low 3 bits, which do not change.
+// the swizzle term depends only on the row's low 4 bits, which do not change.
 struct LaneOffsets {
   int fa0, fa1;   // A fragment chunks (2*q4, 2*q4+1) of row wr + r16
   int fw0, fw1;   // W fragment chunks of row wc + r16
-  int st4a, st4b; // staging stores, 4-bit path: chunks (2*part, 2*part+1) of row tid/4
-  int st8;        // staging store, 8-bit activations: chunk tid%8 of row tid/8
 };
 
 __device__ __forceinline__ LaneOffsets lane_offsets() {
@@ -109,36 +109,8 @@ __device__ __forceinline__ LaneOffsets lane_offsets() {
   o.fa1 = swz(wr + r16, 2 * q4 + 1);
   o.fw0 = kA + swz(wc + r16, 2 * q4);
   o.fw1 = kA + swz(wc + r16, 2 * q4 + 1);
-  o.st4a = swz(tid >> 2, 2 * (tid & 3));
-  o.st4b = swz(tid >> 2, 2 * (tid & 3) + 1);
-  o.st8 = swz(tid >> 3, tid & 7);
+  (void)tid;
   return o;
-}
-
-// Per-lane global offsets of one output tile (rows and columns clamped into
-// range, so edge tiles never read out of bounds; clamped rows and columns
-// compute values that are never stored).
-struct TileOffsets {
-  uint32_t a4[2];  // A_packed 4-bit block: row (tid/4 + 128 i) * 64 + (tid%4) * 16
-  uint32_t a8[4];  // A_packed 8-bit block: row (tid/8 + 64 i) * 128 + (tid%8) * 16
-  uint32_t w[2];   // W_packed: col (tid/4 + 128 i) * K/2 + (tid%4) * 16
-  uint32_t s;      // scale index: row (tid < 256) or column (tid >= 256)
-};
-
-__device__ __forceinline__ TileOffsets tile_offsets(const GemmArgs& p, int m0, int n0) {
-  const int tid = threadIdx.x;
-  TileOffsets t;
-  #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    t.a4[i] = (uint32_t)min(m0 + (tid >> 2) + 128 * i, p.M - 1) * 64u + (tid & 3) * 16u;
-    t.w[i] = (uint32_t)min(n0 + (tid >> 2) + 128 * i, p.N - 1) * (uint32_t)(p.K / 2) +
-             (tid & 3) * 16u;
-  }
-  #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    t.a8[i] = (uint32_t)min(m0 + (tid >> 3) + 64 * i, p.M - 1) * 128u + (tid & 7) * 16u;
-  t.s = tid < kTileM ? (uint32_t)min(m0 + tid, p.M - 1) : (uint32_t)min(n0 + tid - kTileM, p.N - 1);
-  return t;
 }
 
 // One K-block position of the schedule, decoded from the host's encoding:
@@ -159,50 +131,66 @@ struct Stage {
   uint32_t s;
 };
 
-__device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, const TileOffsets& t,
-                                  Stage& st) {
+// Global loads of one K-block's packed operands for the tile at (m0, n0).
+// Rows and columns are clamped into range, so edge tiles never read out of
+// bounds; clamped rows and columns compute values that are never stored.
+__device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, int m0, int n0,
+                                           Stage& st) {
+  const int tid = threadIdx.x;
   const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)kb.aoff;
-  // two loads per lane for a 4-bit block, four for an 8-bit one; the first
-  // two only switch offsets (a select, not a branch, keeps st in registers)
-  const uint32_t sel = 0u - (uint32_t)kb.b8;
+  // 4-bit block: lane chunk tid%4 of rows tid/4 + 128 i (i < 2), 64 bytes a row;
+  // 8-bit block: lane chunk tid%8 of rows tid/8 + 64 i (i < 4), 128 bytes a row.
+  // The first two loads only switch offsets (arithmetic select, so that the
+  // staging registers are not forced into memory by a branch merge).
+  const uint32_t b8 = kb.b8 ? 1u : 0u;
   #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const uint32_t off = t.a4[i] ^ ((t.a4[i] ^ t.a8[i]) & sel);
+    const int r = b8 ? (tid >> 3) + 64 * i : (tid >> 2) + 128 * i;
+    const uint32_t row = (uint32_t)min(m0 + r, p.M - 1);
+    const uint32_t off = (row << (6 + b8)) + ((uint32_t)tid & (3u | (b8 << 2))) * 16u;
     st.a[i] = *reinterpret_cast<const u32x4*>(A + off);
   }
   if (kb.b8) {
     #pragma unroll
-    for (int i = 2; i < 4; ++i) st.a[i] = *reinterpret_cast<const u32x4*>(A + t.a8[i]);
+    for (int i = 2; i < 4; ++i) {
+      const uint32_t row = (uint32_t)min(m0 + (tid >> 3) + 64 * i, p.M - 1);
+      st.a[i] = *reinterpret_cast<const u32x4*>(A + row * 128u + (tid & 7) * 16u);
+    }
   }
   const uint8_t* W = p.W + (size_t)kb.g * 64;
   #pragma unroll
-  for (int i = 0; i < 2; ++i) st.w[i] = *reinterpret_cast<const u32x4*>(W + t.w[i]);
-  if (threadIdx.x < kTileM)
-    st.s = p.sa[(size_t)kb.g * p.M + t.s];
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t col = (uint32_t)min(n0 + (tid >> 2) + 128 * i, p.N - 1);
+    st.w[i] = *reinterpret_cast<const u32x4*>(W + col * (uint32_t)(p.K / 2) + (tid & 3) * 16u);
+  }
+  if (tid < kTileM)
+    st.s = p.sa[(size_t)kb.g * p.M + min(m0 + tid, p.M - 1)];
   else
-    st.s = p.sw[(size_t)kb.g * p.N + t.s];
+    st.s = p.sw[(size_t)kb.g * p.N + min(n0 + tid - kTileM, p.N - 1)];
 }
 
-__device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* buf, const LaneOffsets& o) {
+__device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* buf) {
   const int tid = threadIdx.x;
+  const int st4a = swz(tid >> 2, 2 * (tid & 3)), st4b = swz(tid >> 2, 2 * (tid & 3) + 1);
+  const int st8 = swz(tid >> 3, tid & 7);
   if (!b8) {
     #pragma unroll
     for (int i = 0; i < 2; ++i) {
       u32x4 lo, hi;
       unpack4(st.a[i], lo, hi);
-      *reinterpret_cast<u32x4*>(buf + o.st4a + i * 16384) = lo;
-      *reinterpret_cast<u32x4*>(buf + o.st4b + i * 16384) = hi;
+      *reinterpret_cast<u32x4*>(buf + st4a + i * 16384) = lo;
+      *reinterpret_cast<u32x4*>(buf + st4b + i * 16384) = hi;
     }
   } else {
     #pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + o.st8 + i * 8192) = st.a[i];
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + st8 + i * 8192) = st.a[i];
   }
   #pragma unroll
   for (int i = 0; i < 2; ++i) {
     u32x4 lo, hi;
     unpack4(st.w[i], lo, hi);
-    *reinterpret_cast<u32x4*>(buf + kA + o.st4a + i * 16384) = lo;
-    *reinterpret_cast<u32x4*>(buf + kA + o.st4b + i * 16384) = hi;
+    *reinterpret_cast<u32x4*>(buf + kA + st4a + i * 16384) = lo;
+    *reinterpret_cast<u32x4*>(buf + kA + st4b + i * 16384) = hi;
   }
   // Scales, permuted so that each lane later reads its values with one or two
   // 16-byte LDS reads.  Activation scale of tile row r = 128h + 16rb + 4j + i
@@ -238,17 +226,24 @@ __device__ __forceinline__ void compute_block(const uint8_t* buf, const LaneOffs
   // this lane's 4x4x1 operands: activation scale of row wr + 16rb + 4*q4 + (lane & 3)
   // for every rb, weight scale of column wc + 16cb + r16 for every cb
   const float* scales = reinterpret_cast<const float*>(buf + kA + kW);
-  const f32x4 sal0 = *reinterpret_cast<const f32x4*>(scales + (16 * (wave >> 2) + 4 * q4 + (lane & 3)) * 8);
-  const f32x4 sal1 = *reinterpret_cast<const f32x4*>(scales + (16 * (wave >> 2) + 4 * q4 + (lane & 3)) * 8 + 4);
+  const float* sal = scales + (16 * (wave >> 2) + 4 * q4 + (lane & 3)) * 8;
   const f32x4 swl = *reinterpret_cast<const f32x4*>(scales + kTileM + (16 * (wave & 3) + r16) * 4);
 
   i32x8 wf[kCB];
   #pragma unroll
   for (int cb = 0; cb < kCB; ++cb) wf[cb] = lds_frag(buf + o.fw0 + cb * 2048, buf + o.fw1 + cb * 2048);
+  // the A fragment and activation scale of row block rb + 1 are fetched while
+  // row block rb computes
+  i32x8 an = lds_frag(buf + o.fa0, buf + o.fa1);
+  float san = sal[0];
   #pragma unroll
   for (int rb = 0; rb < kRB; ++rb) {
-    i32x8 af = lds_frag(buf + o.fa0 + rb * 2048, buf + o.fa1 + rb * 2048);
-    const float sa_rb = rb < 4 ? sal0[rb & 3] : sal1[rb & 3];
+    i32x8 af = an;
+    const float sa_rb = san;
+    if (rb + 1 < kRB) {
+      an = lds_frag(buf + o.fa0 + (rb + 1) * 2048, buf + o.fa1 + (rb + 1) * 2048);
+      san = sal[rb + 1];
+    }
     i32x8 ah;
     if constexpr (B8) {
       #pragma unroll
@@ -295,7 +290,7 @@ __device__ __forceinline__ void compute_block(const uint8_t* buf, const LaneOffs
 // precision) is loaded into registers and then stored to the other buffer.
 template <bool DIAG, bool B8>
 __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o,
-                                      const TileOffsets& t, uint8_t* smem, int g_begin, int pos,
+                                      uint8_t* smem, int g_begin, int pos,
                                       int end, int g_end, int NG, int m0, int n0, Stage& st,
                                       f32x4 (&C)[kRB][kCB]) {
   for (; pos < end; ++pos) {
@@ -303,9 +298,9 @@ __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o,
     const bool more = pos + 1 < g_end;
     const KBlock kb = kblock(p.order[pos]);
     const KBlock kn = kblock(p.order[more ? pos + 1 : pos]);
-    if (more) stage_load(p, kn, t, st);
+    if (more) stage_load(p, kn, m0, n0, st);
     compute_block<DIAG, B8>(smem + cur * kBuf, o, kb.g, NG, m0, n0, p, C);
-    if (more) stage_store(st, kn.b8, smem + (cur ^ 1) * kBuf, o);
+    if (more) stage_store(st, kn.b8, smem + (cur ^ 1) * kBuf);
     __syncthreads();
   }
 }
@@ -325,7 +320,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
     const WorkUnit unit = p.units[u];
     const int tm = unit.tile / p.tiles_n, tn = unit.tile % p.tiles_n;
     const int m0 = tm * kTileM, n0 = tn * kTileN;
-    const TileOffsets t = tile_offsets(p, m0, n0);
 
     f32x4 C[kRB][kCB];
     #pragma unroll
@@ -337,13 +331,13 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
     // 4-bit blocks before the 8-bit ones, so each precision runs its own loop
     Stage st;
     const KBlock k0 = kblock(p.order[unit.g_begin]);
-    stage_load(p, k0, t, st);
-    stage_store(st, k0.b8, smem, o);
+    stage_load(p, k0, m0, n0, st);
+    stage_store(st, k0.b8, smem);
     __syncthreads();
     const int split = min(max(p.n4, unit.g_begin), unit.g_end);
-    kloop<DIAG, false>(p, o, t, smem, unit.g_begin, unit.g_begin, split, unit.g_end, NG, m0, n0,
+    kloop<DIAG, false>(p, o, smem, unit.g_begin, unit.g_begin, split, unit.g_end, NG, m0, n0,
                        st, C);
-    kloop<DIAG, true>(p, o, t, smem, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0, n0, st,
+    kloop<DIAG, true>(p, o, smem, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0, n0, st,
                       C);
     if (DIAG) continue;
 
