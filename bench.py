@@ -33,6 +33,8 @@ PEAK_HBM_GBS = 8000.0
 WORKLOADS = {
     "llama3-70b-prefill": dict(M=4096, layers="LLAMA3_70B"),
     "llama3-8b-prefill": dict(M=2048, layers="LLAMA3_8B"),
+    # few-token regime: the gate_up layer streams its 4-bit weights from HBM
+    "llama3-70b-decode": dict(M=8, layers="LLAMA3_70B", only="gate_up", rotate=6),
 }
 
 
@@ -43,6 +45,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama3-70b-prefill", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--m", type=int, default=0, help="tokens (default: the workload's)")
     ap.add_argument("--frac8", type=float, default=1 / 16)
     ap.add_argument("--layers", default="",
                     help="comma-separated subset of the workload's layers (default: all)")
@@ -69,8 +72,11 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     wl = WORKLOADS[args.workload]
-    M = wl["M"]
+    M = args.m or wl["M"]
     shapes = getattr(synth, wl["layers"])
+    if "only" in wl:
+        shapes = {wl["only"]: shapes[wl["only"]]}
+    rotate = wl.get("rotate", 1)
     layers = []
     t_setup = time.time()
     wanted = [x for x in args.layers.split(",") if x] or list(shapes)
@@ -87,23 +93,31 @@ def main():
         Wp, sw = comet.pack_w4(Wd)
         torch.cuda.synchronize()
         del Wd
+        # several weight copies, used in turn, so that each call streams its
+        # weights from HBM instead of the 256 MB last-level cache
+        Wps = [Wp] + [Wp.clone() for _ in range(rotate - 1)]
+        sws = [sw] + [sw.clone() for _ in range(rotate - 1)]
         nbytes = comet.comet_act_packed_bytes(prec, M, K)
         A = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         sa = torch.empty((NG, M), dtype=torch.float16, device=dev)
         out = torch.empty((M, N), dtype=torch.float16, device=dev)
         layers.append(dict(name=name, M=M, N=N, K=K, prec=prec, X=X, X16=X16, W16=W16, Wp=Wp,
-                           sw=sw, A=A, sa=sa, out=out, n8=n8))
+                           sw=sw, Wps=Wps, sws=sws, A=A, sa=sa, out=out, n8=n8))
     t_setup = time.time() - t_setup
 
+    calls = [0]
+
     def step(ev=None):
+        calls[0] += 1
         for i, L in enumerate(layers):
+            j = calls[0] % rotate
             if ev is not None:
                 ev[i][0].record()
             comet.comet_fmpq_quantize_act(L["X"], L["prec"], L["A"], L["sa"], L["M"], L["K"])
             if ev is not None:
                 ev[i][1].record()
-            comet.comet_w4ax_gemm(L["A"], L["prec"], L["sa"], L["Wp"], L["sw"], L["out"], L["M"],
-                                  L["N"], L["K"])
+            comet.comet_w4ax_gemm(L["A"], L["prec"], L["sa"], L["Wps"][j], L["sws"][j], L["out"],
+                                  L["M"], L["N"], L["K"])
             if ev is not None:
                 ev[i][2].record()
 
@@ -140,8 +154,15 @@ def main():
     g_ms /= args.steps
 
     ops = np.array([2.0 * L["M"] * L["N"] * L["K"] for L in layers])
+    # algorithmic HBM bytes of one GEMM call: packed weights and their scales,
+    # packed activations and their scales, fp16 output
+    gbytes = []
+    for L in layers:
+        K, N, NG, k8 = L["K"], L["N"], L["K"] // 128, L["n8"] * 128
+        gbytes.append(N * K / 2 + 2 * N * NG + M * ((K - k8) / 2 + k8) + 2 * M * NG + 2 * M * N)
+    gbytes = np.array(gbytes)
     value = float(ops.sum() / (ms_per_step * 1e-3) / 1e12)
-    achieved = float(ops.sum() / (g_ms.sum() * 1e-3) / 1e12)
+    hbm_bound = "decode" in args.workload
     per_layer = {}
     for i, L in enumerate(layers):
         K, N = L["K"], L["N"]
@@ -152,9 +173,19 @@ def main():
             "K": K, "N": N, "gemm_us": round(g_ms[i] * 1e3, 2),
             "gemm_tops": round(ops[i] / (g_ms[i] * 1e-3) / 1e12, 1),
             "gemm_frac_peak": round(ops[i] / (g_ms[i] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+            "gemm_gbs": round(gbytes[i] / (g_ms[i] * 1e-3) / 1e9, 1),
             "quant_us": round(q_ms[i] * 1e3, 2),
             "quant_gbs": round(qbytes / (q_ms[i] * 1e-3) / 1e9, 1),
         }
+    if hbm_bound:
+        achieved = float(gbytes.sum() / (g_ms.sum() * 1e-3) / 1e9)
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    else:
+        achieved = float(ops.sum() / (g_ms.sum() * 1e-3) / 1e12)
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_MFMA_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": None}
+    roof["kernel"] = "w4ax_gemm (average over the layer launches of a step)"
 
     record = {
         "metric": "W4Ax GEMM effective TOPS (LLaMA-3-70B prefill linear layers)",
@@ -170,19 +201,17 @@ def main():
         "dtype": "fp8",
         "data": "synthetic",
         "config": {
-            "workload": f"{args.workload}: quantize+W4Ax GEMM of qkv/o/gate_up/down at M={M} "
+            "workload": f"{args.workload}: quantize+W4Ax GEMM of {'/'.join(per_layer)} at M={M} "
                         f"tokens, G=128, {args.frac8:.4g} of activation blocks 8-bit",
             "M": M, "G": 128, "frac8": args.frac8, "seed": args.seed,
             "operands": "int4 weights, int4/int8 activation codes on FP8-E4M3 MFMA, fp32 dequant",
         },
-        "roofline": {
-            "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_MFMA_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": None,
-            "kernel": "w4ax_gemm (ops-weighted over the four layer launches)",
-        },
+        "roofline": roof,
         "layers": per_layer,
         "setup_s": round(t_setup, 1),
     }
+    if args.workload != "llama3-70b-prefill":
+        record["metric"] = f"W4Ax GEMM effective TOPS ({args.workload})"
 
     if args.copy_mib > 0:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)

@@ -15,11 +15,12 @@ OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcomet.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["quantize.hip", "gemm.hip", "scheduler.cpp", "comet_api.cpp"]
+SOURCES = ["quantize.hip", "gemm.hip", "gemm_skinny.hip", "scheduler.cpp", "comet_api.cpp"]
 
 # The GEMM's inner loop interleaves MFMAs with the dequantization FMAs: keep
 # MFMA results in VGPRs (no accumulator-register copies).
-PER_FILE = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+PER_FILE = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+            "gemm_skinny.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off", "-fvisibility=hidden",
           "-I" + os.path.join(os.path.dirname(HERE), "include")]

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -136,8 +137,9 @@ struct DevicePlan {
 
 struct Workspace {
   float* partials = nullptr;
-  size_t partial_slots = 0;
+  size_t partial_floats = 0;
   int* counters = nullptr;
+  size_t ncounters = 0;
 };
 
 std::map<PlanKey, DevicePlan> g_plans;
@@ -191,6 +193,10 @@ comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* pr
     std::vector<int> n8_before(h.order.size() + 1, 0);
     for (size_t g = 0; g < h.order.size(); ++g) n8_before[g + 1] = n8_before[g] + (prec[g] == 8);
     for (int g : h.order) blob.push_back(g | (prec[g] == 8) << 10 | (g + n8_before[g]) << 11);
+    // kernels prefetch fixed-size batches past the end of a range; the padding
+    // repeats the last entry so that such reads stay valid block addresses
+    const int last = blob.back();
+    blob.insert(blob.end(), comet::kOrderPad, last);
   }
   const size_t o_split = blob.size();
   blob.insert(blob.end(), h.split_base.begin(), h.split_base.end());
@@ -219,33 +225,38 @@ comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* pr
   return COMET_OK;
 }
 
-// Split-tile workspace of (device, stream), grown to `slots` partial tiles.
-// Caller holds g_mu.
-comet_status_t get_workspace(int dev, hipStream_t stream, size_t slots, Workspace** out) {
+// Split workspace of (device, stream): fp32 partials and arrival counters,
+// grown on demand.  Counters start at zero and every launch leaves them at
+// zero.  Caller holds g_mu.
+comet_status_t get_workspace(int dev, hipStream_t stream, size_t partial_floats, size_t counters,
+                             Workspace** out) {
   Workspace& ws = g_ws[{dev, stream}];
-  if (slots > ws.partial_slots) {
+  if (partial_floats > ws.partial_floats || counters > ws.ncounters) {
     if (ws.partials) {
       // the previous launch on this stream may still use them
       hipError_t e = hipStreamSynchronize(stream);
       if (e != hipSuccess) return fail(COMET_ERR_HIP, "workspace sync: %s", hipGetErrorString(e));
       (void)hipFree(ws.partials);
       (void)hipFree(ws.counters);
-      ws = Workspace{};
     }
-    const size_t tile = (size_t)comet::kTileM * comet::kTileN * sizeof(float);
-    hipError_t e = hipMalloc(&ws.partials, slots * tile);
+    const size_t nf = std::max(partial_floats, ws.partial_floats);
+    const size_t nc = std::max(counters, ws.ncounters);
+    ws = Workspace{};
+    if (std::getenv("COMET_TEST_FAIL_ALLOC")) return fail(COMET_ERR_OOM, "workspace allocation failed (forced)");
+    hipError_t e = hipMalloc(&ws.partials, std::max<size_t>(nf, 1) * sizeof(float));
     if (e != hipSuccess) {
       ws = Workspace{};
       return fail(COMET_ERR_OOM, "workspace allocation: %s", hipGetErrorString(e));
     }
-    e = hipMalloc(&ws.counters, slots * sizeof(int));
-    if (e == hipSuccess) e = hipMemsetAsync(ws.counters, 0, slots * sizeof(int), stream);
+    e = hipMalloc(&ws.counters, std::max<size_t>(nc, 1) * sizeof(int));
+    if (e == hipSuccess) e = hipMemsetAsync(ws.counters, 0, std::max<size_t>(nc, 1) * sizeof(int), stream);
     if (e != hipSuccess) {
       (void)hipFree(ws.partials);
       ws = Workspace{};
       return fail(COMET_ERR_OOM, "workspace counters: %s", hipGetErrorString(e));
     }
-    ws.partial_slots = slots;
+    ws.partial_floats = nf;
+    ws.ncounters = nc;
   }
   *out = &ws;
   return COMET_OK;
@@ -266,16 +277,20 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
     g_attr_set[dev] = true;
   }
   const bool diag = acc != nullptr;
+  const bool skinny = M <= comet::kSkinnyMaxM;
   const DevicePlan* plan;
-  // the diagnostic form always runs whole tiles (no split partials)
+  // the diagnostic form of the tile kernel runs whole tiles (no split partials)
   if ((st = get_plan(dev, info.cus, M, N, K, prec, map, diag ? std::string("dp") : sched_mode(),
                      stream, &plan)))
     return st;
-  Workspace* ws = nullptr;
-  if (plan->host.partial_slots > 0 &&
-      (st = get_workspace(dev, stream, (size_t)plan->host.partial_slots, &ws)))
-    return st;
   comet::GemmArgs a{};
+  a.splits = skinny ? comet::skinny_splits(N, K, info.cus) : 1;
+  Workspace* ws = nullptr;
+  if (!skinny && plan->host.partial_slots > 0) {
+    const size_t slots = (size_t)plan->host.partial_slots;
+    if ((st = get_workspace(dev, stream, slots * comet::kTileM * comet::kTileN, slots, &ws)))
+      return st;
+  }
   a.A = A;
   a.sa = sa;
   a.W = W;
@@ -299,6 +314,7 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   a.win_n0 = n0;
   a.win_n1 = n1;
   a.map = map;
+  if (skinny) return launched(comet::launch_gemm_skinny(a, diag, stream), "gemm launch");
   return launched(comet::launch_gemm(a, plan->host.num_wgs, diag, stream), "gemm launch");
 }
 

@@ -35,17 +35,11 @@
 #include <stdint.h>
 
 #include "kernels.h"
+#include "operand.h"
 
 namespace comet {
 
 namespace {
-
-typedef int i32x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-constexpr uint32_t kSignMag = 0x87878787u;
-constexpr float kUnit = 262144.0f;  // 2^18: (2^-9)^2 of the FP8 code encoding
 
 constexpr int kThreads = 512;            // 8 waves
 constexpr int kWM = 128, kWN = 64;       // wave quadrant
@@ -56,24 +50,6 @@ constexpr int kBuf = kA + kW + 4 * kTileM + 4 * kTileN;
 constexpr int kLds = 2 * kBuf;
 
 static_assert(kTileM == 2 * kWM && kTileN == 4 * kWN, "8 waves as 2 x 4 quadrants");
-
-__device__ __forceinline__ uint32_t rotr4(uint32_t w) { return __builtin_amdgcn_alignbit(w, w, 4); }
-
-// 16 bytes of 4-bit codes (32 channels) -> 32 FP8 bytes, natural channel order.
-__device__ __forceinline__ void unpack4(u32x4 v, u32x4& lo, u32x4& hi) {
-  lo = u32x4{v[0] & kSignMag, rotr4(v[0]) & kSignMag, v[1] & kSignMag, rotr4(v[1]) & kSignMag};
-  hi = u32x4{v[2] & kSignMag, rotr4(v[2]) & kSignMag, v[3] & kSignMag, rotr4(v[3]) & kSignMag};
-}
-
-// 8-bit codes -> FP8 of the high part (|code| >> 3, signed) and low part (|code| & 7, signed).
-__device__ __forceinline__ uint32_t hi8(uint32_t w) { return ((w >> 3) & 0x0F0F0F0Fu) | (w & 0x80808080u); }
-__device__ __forceinline__ uint32_t lo8(uint32_t w) { return w & kSignMag; }
-
-__device__ __forceinline__ f32x4 mfma_fp8(const i32x8& a, const i32x8& b, f32x4 c) {
-  // cbsz = blgp = 0: both operands OCP FP8-E4M3; zero scale operands select
-  // the unscaled instruction.
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
-}
 
 // LDS layout of one stage buffer: A (kTileM rows x 128 B), W (kTileN rows x
 // 128 B), then the tile's fp32 activation scales (times 2^18) and weight
@@ -206,12 +182,6 @@ __device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* b
     const int c = tid - kTileM, q = c >> 6, cb = (c >> 4) & 3, x = c & 15;
     scales[kTileM + (16 * q + x) * 4 + cb] = f;
   }
-}
-
-__device__ __forceinline__ f32x4 scale_products(float sa, float sw) {
-  // lane l receives sa(lane 4*(l/4) + i) * sw(lane l) for i = 0..3, which with
-  // the operand lanes chosen in compute_block is the 16x16 accumulator layout
-  return __builtin_amdgcn_mfma_f32_4x4x1f32(sa, sw, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
 }
 
 template <bool DIAG, bool B8>

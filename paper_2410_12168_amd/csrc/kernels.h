@@ -9,6 +9,7 @@ namespace comet {
 
 constexpr int kG = 128;          // block size along K (the paper's k = 128)
 constexpr int kMaxBlocks = 512;  // blocks per row supported by the bit map (K <= 65536)
+constexpr int kOrderPad = 16;    // entries after the K-block order that repeat its last entry
 
 // Precision of every K-block as a bit set (bit g = 1: block g is 8-bit),
 // passed by value as a kernel argument so no device table is needed.
@@ -37,11 +38,12 @@ struct GemmArgs {
   int* counters;      // per split tile arrival counters (zero between launches)
   const WorkUnit* units;
   const int* wg_begin;
-  const int* order;   // K-block schedule, K/G entries: g | is8 << 10 | (g + 8-bit blocks before g) << 11
+  const int* order;   // K-block schedule, K/G (+ kOrderPad) entries: g | is8 << 10 | (g + 8-bit blocks before g) << 11
   int n4;             // number of 4-bit blocks (they come first in `order`)
   const int* split_index;  // tile -> index into the partial/counter arrays (-1: not split)
   int M, N, K;
   int tiles_n;        // tiles along N
+  int splits;         // split-K slots per column block (few-token kernel)
   int win_m0, win_m1, win_n0, win_n1;
   BlockMap map;
 };
@@ -57,6 +59,13 @@ constexpr int kTileN = 256;
 
 // Persistent GEMM: `num_wgs` workgroups walk a.units (a.wg_begin per group).
 hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, hipStream_t stream);
+// Few-token kernel (M <= kSkinnyMaxM): one wave per (16 columns, split-K slot).
+constexpr int kSkinnyMaxM = 64;
+hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
+// Split-K slots for the few-token kernel: spread the (N/16 x slots) waves
+// evenly over the device's SIMDs.
+int skinny_splits(int N, int K, int cus);
+
 // Allows the GEMM's dynamic LDS size; once per process and device.
 hipError_t set_gemm_attributes();
 int gemm_lds_bytes();

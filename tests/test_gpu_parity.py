@@ -154,3 +154,39 @@ def test_llama3_70b_full_size_sampled_rows(layer):
     ref = oracle.dequant_gemm(qa, sa, qw, sw)
     out = host_u16(r["out"]).view(np.float16)[rows]
     assert_out_close(out, ref, f"70B {layer}")
+
+
+SKINNY = [
+    # few-token shapes (weight-streaming kernel): ragged M, split-K, both precisions
+    (1, 64, 256, "cfg0"),
+    (5, 160, 1024, "random"),
+    (16, 512, 512, "all8"),
+    (33, 96, 1152, "alternate"),
+    (64, 2048, 4096, "cfg0"),
+]
+
+
+@pytest.mark.parametrize("M,N,K,kind", SKINNY)
+def test_skinny_gemm_matches_oracle(M, N, K, kind):
+    prec = make_map(kind, K // 128, seed=M + 1)
+    win = (0, M, max(0, N - 48), N)
+    r = run_path(M, N, K, prec, seed=3 * M + N, diag_window=win)
+    qa, sa = oracle.quantize_act(r["X16"], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    assert np.array_equal(host(r["acc"]), oracle.group_acc(qa, qw[win[2]:win[3]]))
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"{M}x{N}x{K}/{kind}")
+    again = comet.w4ax_gemm(r["A"], prec, r["sa"], r["Wp"], r["sw"], M, N, K)
+    assert torch.equal(r["out"].view(torch.int16), again.view(torch.int16))
+
+
+@pytest.mark.parametrize("M", [1, 8, 32])
+def test_llama3_70b_decode_full_size(M):
+    # LLaMA-3-70B gate_up at decode sizes: every output row checked
+    K, N = synth.LLAMA3_70B["gate_up"]
+    prec = synth.prec_map(K // 128, K // 128 // 16)
+    r = run_path(M, N, K, prec, seed=M)
+    qa, sa = oracle.quantize_act(r["X16"], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"decode M={M}")
