@@ -7,15 +7,20 @@ offline (done once before timing).  Inputs are seeded synthetic tensors of the
 layer shapes, resident in HBM before the timed region starts.
 
 Prints ONE JSON line.  ``value`` is effective TOPS = sum over layers of
-2*M*N*K divided by the step time.  ``roofline`` describes the GEMM kernel
-(ops per launch over its average launch time, measured with HIP events on the
-stream the kernels run on).  ``cpu_baseline`` times the CPU oracle on a
-bounded sample of the same workload (a few token rows of every layer) and also
-checks the GPU output rows of that sample against it.
+2*M*N*K divided by the step time.  ``roofline`` describes the dominant kernel
+launch of the step, the GEMM of the largest layer: its algorithmic ops
+(prefill, MFMA-bound) or bytes (decode, HBM-bound) per launch over its average
+launch time, measured with HIP events on the stream the kernels run on.  Its
+``traffic`` is the HBM bytes per launch read from the rocprofv3 counter
+summary committed under profiles/, reported only while the kernel sources
+still hash to the value recorded there (else null).  ``cpu_baseline`` times
+the CPU oracle on a bounded sample of the same workload (a few token rows of
+every layer) and also checks the GPU output rows of that sample against it.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -30,12 +35,51 @@ sys.path.insert(0, os.path.join(ROOT, "tests"))
 PEAK_MFMA_TFLOPS = 5000.0  # MI355X dense FP8 (= dense INT8) MFMA
 PEAK_HBM_GBS = 8000.0
 
+METRIC = "W4Ax GEMM effective TOPS + % int8-MFMA peak / % HBM BW, LLaMA-3-70B shapes"
+
 WORKLOADS = {
     "llama3-70b-prefill": dict(M=4096, layers="LLAMA3_70B"),
     "llama3-8b-prefill": dict(M=2048, layers="LLAMA3_8B"),
     # few-token regime: the gate_up layer streams its 4-bit weights from HBM
     "llama3-70b-decode": dict(M=8, layers="LLAMA3_70B", only="gate_up", rotate=6),
 }
+
+# Sources that determine each GEMM kernel's code; a counter summary applies
+# only to the sources it was taken with.
+CSRC = os.path.join(ROOT, "paper_2410_12168_amd", "csrc")
+KERNEL_SOURCES = {
+    "tile": ["gemm.hip", "operand.h", "kernels.h"],
+    "skinny": ["gemm_skinny.hip", "operand.h", "kernels.h"],
+}
+SKINNY_MAX_M = 64  # the library runs the few-token kernel up to this M
+
+
+def kernel_sha(kind: str) -> str:
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kind]:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(kind: str, workload: str, layer: str, M: int):
+    """HBM bytes per launch from the committed counter summary of this kernel
+    and workload, or None (no summary, or the kernel changed since)."""
+    path = os.path.join(ROOT, "profiles", f"w4ax_gemm_{kind}_{workload}_{layer}_m{M}.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#")):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("kernel_sources_sha256") != kernel_sha(kind):
+        return None
+    try:
+        return int(float(fields["traffic_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
 
 
 def parse():
@@ -177,18 +221,26 @@ def main():
             "quant_us": round(q_ms[i] * 1e3, 2),
             "quant_gbs": round(qbytes / (q_ms[i] * 1e-3) / 1e9, 1),
         }
+    # the dominant kernel launch: the GEMM of the layer with the most work
+    d = int(np.argmax(ops))
+    D = layers[d]
+    kind = "skinny" if M <= SKINNY_MAX_M else "tile"
     if hbm_bound:
-        achieved = float(gbytes.sum() / (g_ms.sum() * 1e-3) / 1e9)
+        achieved = float(gbytes[d] / (g_ms[d] * 1e-3) / 1e9)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
     else:
-        achieved = float(ops.sum() / (g_ms.sum() * 1e-3) / 1e12)
+        achieved = float(ops[d] / (g_ms[d] * 1e-3) / 1e12)
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_MFMA_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": None}
-    roof["kernel"] = "w4ax_gemm (average over the layer launches of a step)"
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4)}
+    roof["traffic"] = profiled_traffic(kind, args.workload, D["name"], M)
+    roof["kernel"] = (f"w4ax_gemm {kind} kernel, {D['name']} layer (M={M}, K={D['K']}, "
+                      f"N={D['N']}): {'bytes' if hbm_bound else 'ops'} per launch "
+                      f"{int(gbytes[d] if hbm_bound else ops[d])}, {g_ms[d] * 1e3:.2f} us per launch")
+    roof["alg_bytes_per_launch"] = int(gbytes[d])
 
     record = {
-        "metric": "W4Ax GEMM effective TOPS (LLaMA-3-70B prefill linear layers)",
+        "metric": METRIC,
         "value": round(value, 2),
         "unit": "TOPS",
         "n_gpus": 1,
@@ -210,8 +262,6 @@ def main():
         "layers": per_layer,
         "setup_s": round(t_setup, 1),
     }
-    if args.workload != "llama3-70b-prefill":
-        record["metric"] = f"W4Ax GEMM effective TOPS ({args.workload})"
 
     if args.copy_mib > 0:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
