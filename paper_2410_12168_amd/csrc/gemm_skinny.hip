@@ -23,7 +23,7 @@ namespace comet {
 
 namespace {
 
-constexpr int kD = 4;      // K-blocks per load batch
+constexpr int kD = 2;      // K-blocks per load batch (more waves fit than with deeper batches)
 constexpr int kWaves = 4;  // waves per workgroup; the split-K slot count divides it
 
 template <int R, bool B8>

@@ -62,8 +62,9 @@ hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, hipStream_t st
 // Few-token kernel (M <= kSkinnyMaxM): one wave per (16 columns, split-K slot).
 constexpr int kSkinnyMaxM = 64;
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
-// Split-K slots for the few-token kernel: spread the (N/16 x slots) waves
-// evenly over the device's SIMDs.
+// Split-K slots (1, 2 or 4) for the few-token kernel: spread the (N/16 x
+// slots) waves evenly over the device's SIMDs, keeping at least 4 K-blocks per
+// slot.
 int skinny_splits(int N, int K, int cus);
 
 // Allows the GEMM's dynamic LDS size; once per process and device.

@@ -180,9 +180,8 @@ bool build_plan(int M, int N, int K, int G, const uint8_t* prec, const PlanOptio
 
 int skinny_splits(int N, int K, int cus) {
   // waves of (16 columns, slot) over 4 SIMDs per CU: pick the slot count whose
-  // last round of waves is fullest, preferring fewer slots, keeping at least
-  // 4 K-blocks per slot.  The slots of a column block share one workgroup of
-  // four waves, so the count divides 4.
+  // last round of waves is fullest, preferring fewer slots.  The slots of a
+  // column block share one workgroup of four waves, so the count divides 4.
   const int simds = 4 * cus, cblocks = N / 16, NG = K / 128;
   int best = 1;
   double best_eff = 0;

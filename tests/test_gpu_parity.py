@@ -163,6 +163,10 @@ SKINNY = [
     (16, 512, 512, "all8"),
     (33, 96, 1152, "alternate"),
     (64, 2048, 4096, "cfg0"),
+    # four split-K slots per column block; shorter chunks for larger M
+    (8, 512, 2048, "random"),
+    (16, 256, 4096, "cfg0"),
+    (40, 128, 2048, "all8"),
 ]
 
 
