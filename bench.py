@@ -285,12 +285,12 @@ def cpu_baseline(layers, rows_per_layer: int) -> dict:
     from parity import out_errors
 
     threads = os.cpu_count() or 1
-    rows = np.arange(rows_per_layer)
     t_total = 0.0
     ops = 0.0
     worst = 0.0
     worst_norm = 0.0
     for L in layers:
+        rows = np.arange(min(rows_per_layer, L["M"]))
         qw, sw = oracle.quantize_weight(L["W16"], nthreads=threads)  # offline step, not timed
         t0 = time.perf_counter()
         qa, sa = oracle.quantize_act(L["X16"][rows], L["prec"], nthreads=threads)

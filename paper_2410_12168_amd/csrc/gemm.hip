@@ -9,24 +9,27 @@
 // W4A8.  Products of such codes are integers times 2^-18 and their sums stay
 // below 2^24 units, so the fp32 MFMA result is the exact block sum (the
 // paper's integer tile result, Sec. 4.1) and needs no int->float convert.
-// Dequantization (Sec. 4.3: the scale absorbs the conversion factor):
-//     C += Y * P,  P = (sa * 2^18) * sw      in fp32, once per output and K-block.
-// The scale products P of a 16x16 block are one v_mfma_f32_4x4x1_16b_f32
-// (16 outer products of 4 activation scales and 4 weight scales, K = 1, exact
-// in fp32), laid out lane for lane like Y, so the vector ALUs only do the
-// fused multiply-add; they are the co-bottleneck of this kernel.
+// Dequantization (Sec. 4.3: the scale absorbs the conversion factor) runs on
+// the vector ALUs, once per output and K-block:
+//     C += Y * P,   P = (sa * 2^18) * sw      (fp32; sa * sw is exact),
+// two VALU operations per output and K-block: as much vector work as the
+// MFMAs have matrix work.  Each step's dequantization is issued one step
+// late, behind the next step's MFMA, so it never waits for an MFMA result.
 //
 // Kernel structure (the gfx950 form of the paper's software pipeline,
 // Sec. 4.2, and of its tile decomposition, Sec. 4.4):
 //   * persistent workgroups of 8 waves walk a host-built list of work units
 //     (tile, K-block range); full tiles go to one workgroup, the fractional
 //     last wave of tiles is split over all of them by cost;
-//   * per K-block the workgroup stages its 256x256 tile's operands
-//     HBM -> VGPR (128-bit loads) -> unpack -> LDS (double-buffered, XOR
-//     swizzled rows), so every nibble is unpacked once per workgroup, and one
-//     barrier per K-block separates the stages;
-//   * each wave computes a 128x64 quadrant: 8x4 MFMA blocks per K-block, fed
-//     from LDS, with the fp32 dequantization interleaved;
+//   * the tile's packed 4-bit weights stream HBM -> LDS with direct
+//     (register-free) 128-bit loads into a ring of three K-block slots,
+//     issued two K-blocks ahead; each wave unpacks the weight fragments it
+//     uses when it reads them;
+//   * the tile's activation codes and both scale vectors are staged
+//     HBM -> VGPR -> unpack -> LDS one K-block ahead (double-buffered, XOR
+//     swizzled rows), so activation nibbles are unpacked once per workgroup;
+//   * one barrier per K-block separates the stages;
+//   * each wave computes a 128x64 quadrant: 8x4 MFMA blocks per K-block;
 //   * split tiles write fp32 partials; the last workgroup to finish a tile
 //     (arrival counter, no waiting) adds the partials in slot order and
 //     stores fp16, so the result does not depend on arrival order.
@@ -44,20 +47,38 @@ namespace {
 constexpr int kThreads = 512;            // 8 waves
 constexpr int kWM = 128, kWN = 64;       // wave quadrant
 constexpr int kRB = kWM / 16, kCB = kWN / 16;
-constexpr int kA = kTileM * 128;         // LDS bytes of one A stage (fp8 or raw 8-bit codes)
-constexpr int kW = kTileN * 128;         // LDS bytes of one W stage (fp8)
-constexpr int kBuf = kA + kW + 4 * kTileM + 4 * kTileN;
-constexpr int kLds = 2 * kBuf;
+constexpr int kA = kTileM * 128;          // LDS bytes of one A stage (fp8 or raw 8-bit codes)
+constexpr int kS = 4 * (kTileM + kTileN);  // LDS bytes of one stage's scales (fp32)
+constexpr int kBuf = kA + kS;             // one activation stage, double-buffered
+constexpr int kWr = kTileN * 64;          // one packed weight K-block, ring of three
+constexpr int kLds = 2 * kBuf + 3 * kWr;
 
 static_assert(kTileM == 2 * kWM && kTileN == 4 * kWN, "8 waves as 2 x 4 quadrants");
 
-// LDS layout of one stage buffer: A (kTileM rows x 128 B), W (kTileN rows x
-// 128 B), then the tile's fp32 activation scales (times 2^18) and weight
-// scales.  Row r's 16-byte chunk c sits at r*128 + ((c ^ g(r)) << 4) with
-// g(r) = (r ^ (r >> 1)) & 7.  With this swizzle the 16 rows of one MFMA
-// operand fetch (ds_read_b128) are bank-conflict free on gfx950 (measured:
-// the plain c ^ (r & 7) swizzle runs at 60% of the read bandwidth).
+// LDS layout of one activation stage: A (kTileM rows x 128 B), then the
+// tile's fp32 activation scales (times 2^18) and weight scales.  Row r's
+// 16-byte chunk c sits at r*128 + ((c ^ g(r)) << 4) with g(r) = (r ^ (r >> 1))
+// & 7.  With this swizzle the 16 rows of one MFMA operand fetch
+// (ds_read_b128) are bank-conflict free on gfx950 (measured: the plain
+// c ^ (r & 7) swizzle runs at 60% of the read bandwidth).
 __device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ ((r ^ (r >> 1)) & 7)) << 4); }
+
+// Packed weights in a ring slot: column c's 64 bytes (one K-block) at c * 64,
+// its 16-byte chunk j (32 codes) at slot j ^ ((c >> 2) & 3), so that the 16
+// columns read by each 16-lane phase of a ds_read_b128 hit distinct banks.
+__device__ __forceinline__ int wswz(int c, int j) { return c * 64 + ((j ^ ((c >> 2) & 3)) << 4); }
+
+// Scales of one stage (floats after the A codes): the activation scale of
+// tile row r = 128 h + 16 rb + 4 j + i at ((h * 8 + rb) * 4 + j) * 4 + i, so a
+// lane's four rows of a row block are one 16-byte read; the weight scale of
+// tile column c = 64 q + 16 cb + x at kTileM + (16 q + x) * 4 + cb, so a
+// lane's column in all four column blocks is one 16-byte read.
+__device__ __forceinline__ int sa_slot(int r) {
+  return (((r >> 7) * 8 + ((r >> 4) & 7)) * 4 + ((r >> 2) & 3)) * 4 + (r & 3);
+}
+__device__ __forceinline__ int sw_slot(int c) {
+  return kTileM + (16 * (c >> 6) + (c & 15)) * 4 + ((c >> 4) & 3);
+}
 
 __device__ __forceinline__ i32x8 lds_frag(const uint8_t* p0, const uint8_t* p1) {
   const u32x4 x = *reinterpret_cast<const u32x4*>(p0);
@@ -73,7 +94,7 @@ __device__ __forceinline__ i32x8 lds_frag(const uint8_t* p0, const uint8_t* p1) 
 // the swizzle term depends only on the row's low 4 bits, which do not change.
 struct LaneOffsets {
   int fa0, fa1;   // A fragment chunks (2*q4, 2*q4+1) of row wr + r16
-  int fw0, fw1;   // W fragment chunks of row wc + r16
+  int fw;         // packed weight chunk q4 of column wc + r16 (in a ring slot)
 };
 
 __device__ __forceinline__ LaneOffsets lane_offsets() {
@@ -83,8 +104,7 @@ __device__ __forceinline__ LaneOffsets lane_offsets() {
   LaneOffsets o;
   o.fa0 = swz(wr + r16, 2 * q4);
   o.fa1 = swz(wr + r16, 2 * q4 + 1);
-  o.fw0 = kA + swz(wc + r16, 2 * q4);
-  o.fw1 = kA + swz(wc + r16, 2 * q4 + 1);
+  o.fw = wswz(wc + r16, q4);
   (void)tid;
   return o;
 }
@@ -100,14 +120,15 @@ struct KBlock {
 
 __device__ __forceinline__ KBlock kblock(int e) { return KBlock{e & 1023, ((e >> 10) & 1) != 0, e >> 11}; }
 
-// Registers holding one K-block's packed operands between load and LDS store.
+// Registers holding one K-block's activation codes and a scale between load
+// and LDS store.
 struct Stage {
   u32x4 a[4];
-  u32x4 w[2];
   uint32_t s;
 };
 
-// Global loads of one K-block's packed operands for the tile at (m0, n0).
+// Global loads of one K-block's activation codes and scales for the tile at
+// (m0, n0).
 // Rows and columns are clamped into range, so edge tiles never read out of
 // bounds; clamped rows and columns compute values that are never stored.
 __device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, int m0, int n0,
@@ -133,12 +154,6 @@ __device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, 
       st.a[i] = *reinterpret_cast<const u32x4*>(A + row * 128u + (tid & 7) * 16u);
     }
   }
-  const uint8_t* W = p.W + (size_t)kb.g * 64;
-  #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const uint32_t col = (uint32_t)min(n0 + (tid >> 2) + 128 * i, p.N - 1);
-    st.w[i] = *reinterpret_cast<const u32x4*>(W + col * (uint32_t)(p.K / 2) + (tid & 3) * 16u);
-  }
   if (tid < kTileM)
     st.s = p.sa[(size_t)kb.g * p.M + min(m0 + tid, p.M - 1)];
   else
@@ -161,117 +176,178 @@ __device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* b
     #pragma unroll
     for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + st8 + i * 8192) = st.a[i];
   }
+  const float f = __half2float(__ushort_as_half((unsigned short)st.s));
+  float* scales = reinterpret_cast<float*>(buf + kA);
+  if (tid < kTileM)
+    scales[sa_slot(tid)] = f * kUnit;
+  else
+    scales[sw_slot(tid - kTileM)] = f;
+}
+
+// Direct global -> LDS load of 16 bytes per lane: the wave's 64 chunks land
+// at LDS bytes lds .. lds + 1023, lane by lane.  Issued as inline assembly so
+// that the compiler does not wait for it at LDS reads of other ring slots;
+// the K-loop waits for it explicitly before the barrier that publishes it.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Packed weights of K-block g for the tile's 256 columns into a ring slot:
+// 16 KB, two 1 KB wave loads per wave.  Lane L of load j fills column
+// 16 j + L / 4, slot L % 4, with the chunk that wswz() places there.
+// Columns past N are clamped (their outputs are never stored).
+__device__ __forceinline__ void dma_w(const GemmArgs& p, int g, int n0, uint32_t slot) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
   #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    u32x4 lo, hi;
-    unpack4(st.w[i], lo, hi);
-    *reinterpret_cast<u32x4*>(buf + kA + st4a + i * 16384) = lo;
-    *reinterpret_cast<u32x4*>(buf + kA + st4b + i * 16384) = hi;
-  }
-  // Scales, permuted so that each lane later reads its values with one or two
-  // 16-byte LDS reads.  Activation scale of tile row r = 128h + 16rb + 4j + i
-  // goes to (16h + 4j + i) * 8 + rb (the 8 row blocks of one 4x4x1 operand
-  // lane); weight scale of tile column c = 64q + 16cb + x to
-  // kTileM + (16q + x) * 4 + cb.
-  const float f = __half2float(__ushort_as_half((unsigned short)st.s));
-  float* scales = reinterpret_cast<float*>(buf + kA + kW);
-  if (tid < kTileM) {
-    const int r = tid, h = r >> 7, rb = (r >> 4) & 7, j = (r >> 2) & 3, i = r & 3;
-    scales[(16 * h + 4 * j + i) * 8 + rb] = f * kUnit;
-  } else {
-    const int c = tid - kTileM, q = c >> 6, cb = (c >> 4) & 3, x = c & 15;
-    scales[kTileM + (16 * q + x) * 4 + cb] = f;
+    const int j = 2 * wave + i;
+    const uint32_t col = (uint32_t)min(n0 + 16 * j + (lane >> 2), p.N - 1);
+    const uint8_t* src = p.W + (size_t)col * (uint32_t)(p.K / 2) + (size_t)g * 64 + chunk * 16;
+    dma16(src, slot + j * 1024);
   }
 }
 
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Barrier that publishes this wave's LDS writes (ds_write completion) but
+// leaves its outstanding global loads in flight.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// 16 bytes of 4-bit codes (32 channels) -> one MFMA operand of 32 FP8 bytes.
+__device__ __forceinline__ i32x8 unpack_frag(u32x4 v) {
+  i32x8 f;
+  #pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = (int)(v[i] & kSignMag);
+    f[2 * i + 1] = (int)(rotr4(v[i]) & kSignMag);
+  }
+  return f;
+}
+
+// One K-block of the wave's quadrant: activation stage `buf` (fp8 or raw
+// 8-bit codes, then scales), packed weights in ring slot `wbuf`.
 template <bool DIAG, bool B8>
-__device__ __forceinline__ void compute_block(const uint8_t* buf, const LaneOffsets& o, int g, int NG,
-                                              int m0, int n0, const GemmArgs& p,
-                                              f32x4 (&C)[kRB][kCB]) {
+__device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t* wbuf,
+                                              const LaneOffsets& o, int g, int NG, int m0, int n0,
+                                              const GemmArgs& p, f32x4 (&C)[kRB][kCB]) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r16 = lane & 15, q4 = lane >> 4;
   const int wr = (wave >> 2) * kWM;
   const int wc = (wave & 3) * kWN;
-  // this lane's 4x4x1 operands: activation scale of row wr + 16rb + 4*q4 + (lane & 3)
-  // for every rb, weight scale of column wc + 16cb + r16 for every cb
-  const float* scales = reinterpret_cast<const float*>(buf + kA + kW);
-  const float* sal = scales + (16 * (wave >> 2) + 4 * q4 + (lane & 3)) * 8;
+  // this lane's rows wr + 16 rb + 4 q4 + i (i < 4) and column wc + 16 cb + r16
+  const float* scales = reinterpret_cast<const float*>(buf + kA);
+  const float* sal = scales + ((wave >> 2) * 32 + q4) * 4;  // + 16 rb
   const f32x4 swl = *reinterpret_cast<const f32x4*>(scales + kTileM + (16 * (wave & 3) + r16) * 4);
 
   i32x8 wf[kCB];
   #pragma unroll
-  for (int cb = 0; cb < kCB; ++cb) wf[cb] = lds_frag(buf + o.fw0 + cb * 2048, buf + o.fw1 + cb * 2048);
-  // the A fragment and activation scale of row block rb + 1 are fetched while
-  // row block rb computes
-  i32x8 an = lds_frag(buf + o.fa0, buf + o.fa1);
-  float san = sal[0];
+  for (int cb = 0; cb < kCB; ++cb)
+    wf[cb] = unpack_frag(*reinterpret_cast<const u32x4*>(wbuf + o.fw + cb * 1024));
+  // the A fragment and activation scales of row block rb + 1 are fetched
+  // while row block rb computes
+  i32x8 af = lds_frag(buf + o.fa0, buf + o.fa1);
+  f32x4 san = *reinterpret_cast<const f32x4*>(sal);
+  i32x8 ah;
+  f32x4 sa_rb = san;
+  // Step s = (rb, cb).  The dequantization of step s - 1 is issued after the
+  // MFMA of step s, so the vector ALU works while the matrix core does.
+  f32x4 yq = {0.f, 0.f, 0.f, 0.f}, pq = {0.f, 0.f, 0.f, 0.f};
   #pragma unroll
-  for (int rb = 0; rb < kRB; ++rb) {
-    i32x8 af = an;
-    const float sa_rb = san;
-    if (rb + 1 < kRB) {
-      an = lds_frag(buf + o.fa0 + (rb + 1) * 2048, buf + o.fa1 + (rb + 1) * 2048);
-      san = sal[rb + 1];
+  for (int s = 0; s < kRB * kCB; ++s) {
+    const int rb = s / kCB, cb = s % kCB;
+    if (cb == 0) {
+      sa_rb = san;
+      if (rb + 1 < kRB) san = *reinterpret_cast<const f32x4*>(sal + (rb + 1) * 16);
+      if constexpr (B8) {
+        #pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          ah[i] = (int)hi8((uint32_t)af[i]);
+          af[i] = (int)lo8((uint32_t)af[i]);
+        }
+      }
     }
-    i32x8 ah;
+    f32x4 y = mfma_fp8(af, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
+    f32x4 yh;
+    if constexpr (B8) yh = mfma_fp8(ah, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
+    if (cb == kCB - 1 && rb + 1 < kRB) {
+      // the next row block's fragment replaces this one in the same registers
+      __builtin_amdgcn_sched_barrier(0);
+      af = lds_frag(buf + o.fa0 + (rb + 1) * 2048, buf + o.fa1 + (rb + 1) * 2048);
+    }
     if constexpr (B8) {
       #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        ah[i] = (int)hi8((uint32_t)af[i]);
-        af[i] = (int)lo8((uint32_t)af[i]);
-      }
+      for (int i = 0; i < 4; ++i) y[i] = __builtin_fmaf(yh[i], 8.0f, y[i]);  // exact
     }
-    #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) {
-      f32x4 y = mfma_fp8(af, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
-      if constexpr (B8) {
-        const f32x4 yh = mfma_fp8(ah, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
-        #pragma unroll
-        for (int i = 0; i < 4; ++i) y[i] = __builtin_fmaf(yh[i], 8.0f, y[i]);  // exact
-      }
-      if constexpr (DIAG) {
-        const int col = n0 + wc + cb * 16 + r16;
-        #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = m0 + wr + rb * 16 + 4 * q4 + i;
-          if (row >= p.win_m0 && row < p.win_m1 && col >= p.win_n0 && col < p.win_n1) {
-            const size_t idx = ((size_t)(row - p.win_m0) * (p.win_n1 - p.win_n0) +
-                                (col - p.win_n0)) * NG + g;
-            p.acc[idx] = (int32_t)(y[i] * kUnit);
-          }
+    if constexpr (DIAG) {
+      const int col = n0 + wc + cb * 16 + r16;
+      #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + wr + rb * 16 + 4 * q4 + i;
+        if (row >= p.win_m0 && row < p.win_m1 && col >= p.win_n0 && col < p.win_n1) {
+          const size_t idx = ((size_t)(row - p.win_m0) * (p.win_n1 - p.win_n0) +
+                              (col - p.win_n0)) * NG + g;
+          p.acc[idx] = (int32_t)(y[i] * kUnit);
         }
-      } else {
-        const f32x4 P = scale_products(sa_rb, swl[cb]);
-        #pragma unroll
-        for (int i = 0; i < 4; ++i) C[rb][cb][i] = __builtin_fmaf(y[i], P[i], C[rb][cb][i]);
       }
+    } else {
+      const f32x4 P = sa_rb * swl[cb];  // exact: 11-bit by 11-bit significands
+      if (s > 0) {
+        const int pr = (s - 1) / kCB, pc = (s - 1) % kCB;
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) C[pr][pc][i] = __builtin_fmaf(yq[i], pq[i], C[pr][pc][i]);
+        // pin each row block's updates here; otherwise the optimizer sinks
+        // the FMAs past the barrier and keeps all the K-block's MFMA results
+        // live at once
+        if (pc == kCB - 1)
+          asm volatile("" : "+v"(C[pr][0]), "+v"(C[pr][1]), "+v"(C[pr][2]), "+v"(C[pr][3]));
+      }
+      yq = y;
+      pq = P;
     }
-    // Pin this row block's accumulator updates here.  Without it the
-    // optimizer sinks the FMAs past the barrier into the next K-block, keeping
-    // all 32 MFMA results of the K-block live at once (and spilling them).
-    if constexpr (!DIAG)
-      asm volatile("" : "+v"(C[rb][0]), "+v"(C[rb][1]), "+v"(C[rb][2]), "+v"(C[rb][3]));
+  }
+  if constexpr (!DIAG) {
+    #pragma unroll
+    for (int i = 0; i < 4; ++i)
+      C[kRB - 1][kCB - 1][i] = __builtin_fmaf(yq[i], pq[i], C[kRB - 1][kCB - 1][i]);
+    asm volatile("" : "+v"(C[kRB - 1][0]), "+v"(C[kRB - 1][1]), "+v"(C[kRB - 1][2]),
+                 "+v"(C[kRB - 1][3]));
   }
 }
 
-// Pipelined K-loop over schedule positions [pos, end), all of precision B8:
-// K-block k is computed from one LDS buffer while k+1 (whatever its
-// precision) is loaded into registers and then stored to the other buffer.
+// Pipelined K-loop over schedule positions [pos, end), all of precision B8.
+// Relative position j = pos - g_begin computes from activation stage j % 2
+// and weight ring slot j % 3.  During it, the activation stage of j + 1 is
+// loaded into registers and stored to the other stage, and the weights of
+// j + 2 are loaded straight into ring slot (j + 2) % 3, last read at j - 1.
+// The weights of j + 1 were issued before this iteration's activation loads,
+// so they have arrived once those have (loads complete in order); the wait
+// before the barrier makes that explicit.
 template <bool DIAG, bool B8>
-__device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o,
-                                      uint8_t* smem, int g_begin, int pos,
-                                      int end, int g_end, int NG, int m0, int n0, Stage& st,
-                                      f32x4 (&C)[kRB][kCB]) {
+__device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o, uint8_t* smem,
+                                      uint32_t lds, int g_begin, int pos, int end, int g_end,
+                                      int NG, int m0, int n0, Stage& st, f32x4 (&C)[kRB][kCB]) {
   for (; pos < end; ++pos) {
-    const int cur = (pos - g_begin) & 1;
+    const int j = pos - g_begin;
+    const int cur = j & 1, wslot = j % 3;
     const bool more = pos + 1 < g_end;
     const KBlock kb = kblock(p.order[pos]);
     const KBlock kn = kblock(p.order[more ? pos + 1 : pos]);
     if (more) stage_load(p, kn, m0, n0, st);
-    compute_block<DIAG, B8>(smem + cur * kBuf, o, kb.g, NG, m0, n0, p, C);
+    compute_block<DIAG, B8>(smem + cur * kBuf, smem + 2 * kBuf + wslot * kWr, o, kb.g, NG, m0,
+                            n0, p, C);
     if (more) stage_store(st, kn.b8, smem + (cur ^ 1) * kBuf);
-    __syncthreads();
+    wait_vm_all();
+    if (pos + 2 < g_end) {
+      const int nslot = wslot == 0 ? 2 : wslot - 1;  // (j + 2) % 3
+      dma_w(p, kblock(p.order[pos + 2]).g, n0, lds + 2 * kBuf + nslot * kWr);
+    }
+    barrier_lds();
   }
 }
 
@@ -284,6 +360,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
   const int wave = threadIdx.x >> 6;
   const int r16 = lane & 15, q4 = lane >> 4;
   const LaneOffsets o = lane_offsets();
+  const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
   const int u_end = p.wg_begin[blockIdx.x + 1];
 
   for (int u = p.wg_begin[blockIdx.x]; u < u_end; ++u) {
@@ -301,14 +378,18 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
     // 4-bit blocks before the 8-bit ones, so each precision runs its own loop
     Stage st;
     const KBlock k0 = kblock(p.order[unit.g_begin]);
+    dma_w(p, k0.g, n0, lds + 2 * kBuf);
+    if (unit.g_begin + 1 < unit.g_end)
+      dma_w(p, kblock(p.order[unit.g_begin + 1]).g, n0, lds + 2 * kBuf + kWr);
     stage_load(p, k0, m0, n0, st);
     stage_store(st, k0.b8, smem);
-    __syncthreads();
+    wait_vm_all();
+    barrier_lds();
     const int split = min(max(p.n4, unit.g_begin), unit.g_end);
-    kloop<DIAG, false>(p, o, smem, unit.g_begin, unit.g_begin, split, unit.g_end, NG, m0, n0,
-                       st, C);
-    kloop<DIAG, true>(p, o, smem, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0, n0, st,
-                      C);
+    kloop<DIAG, false>(p, o, smem, lds, unit.g_begin, unit.g_begin, split, unit.g_end, NG, m0,
+                       n0, st, C);
+    kloop<DIAG, true>(p, o, smem, lds, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0, n0,
+                      st, C);
     if (DIAG) continue;
 
     const int wr = (wave >> 2) * kWM, wc = (wave & 3) * kWN;
