@@ -3,11 +3,18 @@
 // With a handful of tokens the GEMM is a weight stream: every 4-bit weight is
 // read from HBM once and used by at most 64 activation rows, so the bound is
 // HBM bandwidth, not the matrix cores.  Each wave owns 16 output columns and
-// a contiguous range of the K-block schedule (split-K slot), loads its weight
-// fragments straight from HBM into registers (no LDS, no sharing), four
-// K-blocks per batch with the next batch in flight while the current one
-// computes, and reads the tiny activation operand through L2.  The operand
-// path is the prefill kernel's: FP8-E4M3 subnormal codes, one
+// a contiguous K-block range (split-K slot), walked in natural block order in
+// batches of four K-blocks.  A batch's weights are 256 contiguous bytes of
+// each of the wave's 16 weight rows: four nontemporal 128-bit loads per lane,
+// each covering 4 rows x 256 bytes (whole cache lines, long runs per row: the
+// fastest read shape measured on MI355X for this layout).  The next batch is
+// in flight while the current one computes.  The wave rearranges each batch
+// into MFMA fragments through a private 4 KB LDS buffer (write as loaded,
+// read per K-block, XOR-swizzled so both sides are bank-conflict free), so
+// no lane shuffles cost vector-ALU time.  The tiny activation operand and
+// the scales are read through L2, one K-block ahead.
+//
+// The operand path is the prefill kernel's: FP8-E4M3 subnormal codes, one
 // v_mfma_f32_16x16x128_f8f6f4 per 16x16 block and K-block (two for 8-bit
 // activation blocks), exact scale products from v_mfma_f32_4x4x1_16b_f32,
 // fp32 FMA dequantization.  Split-K slots of one column block live in one
@@ -23,150 +30,174 @@ namespace comet {
 
 namespace {
 
-constexpr int kD = 2;      // K-blocks per load batch (more waves fit than with deeper batches)
+constexpr int kD = 4;      // K-blocks per weight batch (256 bytes of each weight row)
 constexpr int kWaves = 4;  // waves per workgroup; the split-K slot count divides it
 
-template <int R, bool B8>
-struct Batch {
-  u32x4 w[kD];
-  u32x4 a[kD][R][B8 ? 2 : 1];
-  uint32_t sa[kD][R];  // raw fp16 bits, converted when used (no wait at load time)
-  uint32_t sw[kD];
+// One K-block's activation fragments and scales, loaded one step ahead.  Both
+// 16-byte halves are always loaded (for a 4-bit block the second repeats the
+// first), so every step issues the same loads and the compiler's waits stay
+// partial.
+template <int R>
+struct AStep {
+  u32x4 a[R][2];
+  uint32_t sa[R];  // raw fp16 bits, converted when used
+  uint32_t sw;
 };
 
-// K-block order entry at schedule position `pos` (wave-uniform).  The order
-// array is written once when the plan is built and only read by kernels, so
-// it is read through the constant address space: scalar loads that the
-// issue_point() barriers below do not force back to vector loads (a vector
-// load here would queue behind the weight loads and wait for them).
-typedef const int __attribute__((address_space(4)))* ConstIntPtr;
-__device__ __forceinline__ int order_entry(const GemmArgs& p, int pos) {
-  return ((ConstIntPtr)p.order)[pos];
+// Precision bit of K-block g.
+__device__ __forceinline__ bool is8(const GemmArgs& p, int g) {
+  return (p.map.bits[g >> 6] >> (g & 63)) & 1;
 }
 
-// Loads schedule positions [pos, pos + kD), unconditionally.  Positions past
-// the end of the wave's range read whatever valid block the order holds there
-// (the order array is padded by kOrderPad >= 2 * kD - 1 entries) and are
-// masked in compute_batch.  Unconditional loads keep every wait a partial
-// one: a load under a branch makes the compiler's wait-count merge fall back
-// to waiting for all loads, which serialises the double buffering.
-template <int R, bool B8>
-__device__ __forceinline__ void load_batch(const GemmArgs& p, int pos, int col, Batch<R, B8>& b) {
-  static_assert(kOrderPad >= 2 * kD - 1, "order padding too short for the prefetch depth");
+// Offset of K-block g in A_packed, in units of M * 64 bytes: g plus the
+// 8-bit blocks before it.
+__device__ __forceinline__ int aoff_of(const GemmArgs& p, int g) {
+  int n = 0;
+  for (int w = 0; w < (g >> 6); ++w) n += __popcll(p.map.bits[w]);
+  if (g & 63) n += __popcll(p.map.bits[g >> 6] & ((1ull << (g & 63)) - 1));
+  return g + n;
+}
+
+// Activation fragments (rows 16 r + lane % 16, 32 codes of quarter lane / 16)
+// and scales of K-block g, whose block starts at aoff * M * 64 bytes.
+template <int R>
+__device__ __forceinline__ void load_a(const GemmArgs& p, int g, int aoff, int col, AStep<R>& s) {
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, q4 = lane >> 4;
+  const uint32_t b8 = is8(p, g) ? 1u : 0u;
+  const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)aoff;
   #pragma unroll
-  for (int d = 0; d < kD; ++d) {
-    const int e = order_entry(p, pos + d);
-    const int g = e & 1023, aoff = e >> 11;
-    b.w[d] = *reinterpret_cast<const u32x4*>(p.W + (size_t)col * (p.K / 2) + (size_t)g * 64 + q4 * 16);
-    const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)aoff;
-    #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int row = min(16 * r + r16, p.M - 1);
-      if constexpr (B8) {
-        b.a[d][r][0] = *reinterpret_cast<const u32x4*>(A + (size_t)row * 128 + q4 * 32);
-        b.a[d][r][1] = *reinterpret_cast<const u32x4*>(A + (size_t)row * 128 + q4 * 32 + 16);
-      } else {
-        b.a[d][r][0] = *reinterpret_cast<const u32x4*>(A + (size_t)row * 64 + q4 * 16);
-      }
-      // 4x4x1 operand: activation scale of row 16r + 4*q4 + (lane & 3)
-      const int srow = min(16 * r + 4 * q4 + (lane & 3), p.M - 1);
-      b.sa[d][r] = p.sa[(size_t)g * p.M + srow];
-    }
-    b.sw[d] = p.sw[(size_t)g * p.N + col];
+  for (int r = 0; r < R; ++r) {
+    const uint32_t row = (uint32_t)min(16 * r + r16, p.M - 1);
+    const uint8_t* base = A + (row << (6 + b8)) + ((uint32_t)q4 << (4 + b8));
+    s.a[r][0] = *reinterpret_cast<const u32x4*>(base);
+    s.a[r][1] = *reinterpret_cast<const u32x4*>(base + (b8 << 4));
+    // 4x4x1 operand: activation scale of row 16 r + 4 q4 + (lane & 3)
+    const int srow = min(16 * r + 4 * q4 + (lane & 3), p.M - 1);
+    s.sa[r] = p.sa[(size_t)g * p.M + srow];
+  }
+  s.sw = p.sw[(size_t)g * p.N + col];
+}
+
+// Weights of the batch starting at K-block gb for the wave's 16 rows n0..:
+// load j covers rows 4 j + lane / 16, bytes 16 * (lane % 16) of the row's
+// 256-byte run (K-block gb + (lane % 16) / 4, quarter lane % 4).  K-blocks
+// past the last one repeat it (in-row reads; never computed).
+__device__ __forceinline__ void load_w(const GemmArgs& p, int gb, int n0, u32x4 (&w)[4]) {
+  const int lane = threadIdx.x & 63;
+  const int c = lane & 15;
+  const int g = min(gb + (c >> 2), p.K / kG - 1);
+  #pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = n0 + 4 * j + (lane >> 4);
+    const u32x4* src = reinterpret_cast<const u32x4*>(p.W + (size_t)row * (p.K / 2) +
+                                                      (size_t)g * 64 + (c & 3) * 16);
+    w[j] = __builtin_nontemporal_load(src);
   }
 }
 
-template <int R, bool B8, bool DIAG>
-__device__ __forceinline__ void compute_batch(const GemmArgs& p, int pos, int end, int n0,
-                                              const Batch<R, B8>& b, f32x4 (&C)[R]) {
+// The wave's LDS buffer holds a batch as 16 rows x 256 bytes; row r's 16-byte
+// chunk c (K-block c / 4, quarter c % 4) sits at r * 256 + ((c ^ r) << 4).
+// Writes: 16 lanes fill one row's 256 bytes.  Fragment reads: 16 lanes read
+// 16 rows at one logical chunk, which the XOR spreads over all banks.
+__device__ __forceinline__ void store_w(uint8_t* buf, const u32x4 (&w)[4]) {
+  const int lane = threadIdx.x & 63;
+  const int c = lane & 15;
+  #pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = 4 * j + (lane >> 4);
+    *reinterpret_cast<u32x4*>(buf + row * 256 + ((c ^ row) << 4)) = w[j];
+  }
+}
+
+template <int R, bool DIAG>
+__device__ __forceinline__ void compute_step(const GemmArgs& p, const uint8_t* wbuf, int i,
+                                             int g, bool b8, int n0, const AStep<R>& s,
+                                             f32x4 (&C)[R]) {
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, q4 = lane >> 4;
   const int NG = p.K / kG;
+  const u32x4 wraw = *reinterpret_cast<const u32x4*>(wbuf + r16 * 256 + (((4 * i + q4) ^ r16) << 4));
+  u32x4 wlo, whi;
+  unpack4(wraw, wlo, whi);
+  const i32x8 wf = {(int)wlo[0], (int)wlo[1], (int)wlo[2], (int)wlo[3],
+                    (int)whi[0], (int)whi[1], (int)whi[2], (int)whi[3]};
   #pragma unroll
-  for (int d = 0; d < kD; ++d) {
-    const bool valid = pos + d < end;  // a block past the range contributes zero
-    {
-      u32x4 lo, hi;
-      unpack4(b.w[d], lo, hi);
-      const i32x8 wf = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
-                        (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+  for (int r = 0; r < R; ++r) {
+    f32x4 y;
+    if (b8) {
+      i32x8 al, ah;
       #pragma unroll
-      for (int r = 0; r < R; ++r) {
-        f32x4 y;
-        if constexpr (B8) {
-          i32x8 al, ah;
-          #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            al[i] = (int)lo8(b.a[d][r][0][i]);
-            al[4 + i] = (int)lo8(b.a[d][r][1][i]);
-            ah[i] = (int)hi8(b.a[d][r][0][i]);
-            ah[4 + i] = (int)hi8(b.a[d][r][1][i]);
-          }
-          const f32x4 yh = mfma_fp8(ah, wf, f32x4{0.f, 0.f, 0.f, 0.f});
-          y = mfma_fp8(al, wf, yh * 8.0f);  // exact: integers below 2^24 units
-        } else {
-          u32x4 alo, ahi;
-          unpack4(b.a[d][r][0], alo, ahi);
-          const i32x8 af = {(int)alo[0], (int)alo[1], (int)alo[2], (int)alo[3],
-                            (int)ahi[0], (int)ahi[1], (int)ahi[2], (int)ahi[3]};
-          y = mfma_fp8(af, wf, f32x4{0.f, 0.f, 0.f, 0.f});
-        }
-        if constexpr (DIAG) {
-          if (!valid) continue;
-          const int g = order_entry(p, pos + d) & 1023;
-          const int col = n0 + r16;
-          #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int row = 16 * r + 4 * q4 + i;
-            if (row >= p.win_m0 && row < p.win_m1 && col >= p.win_n0 && col < p.win_n1) {
-              const size_t idx = ((size_t)(row - p.win_m0) * (p.win_n1 - p.win_n0) +
-                                  (col - p.win_n0)) * NG + g;
-              p.acc[idx] = (int32_t)(y[i] * kUnit);
-            }
-          }
-        } else {
-          const float sa = __half2float(__ushort_as_half((unsigned short)b.sa[d][r])) * kUnit;
-          const float sw = valid ? __half2float(__ushort_as_half((unsigned short)b.sw[d])) : 0.0f;
-          const f32x4 P = scale_products(sa, sw);
-          #pragma unroll
-          for (int i = 0; i < 4; ++i) C[r][i] = __builtin_fmaf(y[i], P[i], C[r][i]);
+      for (int k = 0; k < 4; ++k) {
+        al[k] = (int)lo8(s.a[r][0][k]);
+        al[4 + k] = (int)lo8(s.a[r][1][k]);
+        ah[k] = (int)hi8(s.a[r][0][k]);
+        ah[4 + k] = (int)hi8(s.a[r][1][k]);
+      }
+      const f32x4 yh = mfma_fp8(ah, wf, f32x4{0.f, 0.f, 0.f, 0.f});
+      y = mfma_fp8(al, wf, yh * 8.0f);  // exact: integers below 2^24 units
+    } else {
+      u32x4 alo, ahi;
+      unpack4(s.a[r][0], alo, ahi);
+      const i32x8 af = {(int)alo[0], (int)alo[1], (int)alo[2], (int)alo[3],
+                        (int)ahi[0], (int)ahi[1], (int)ahi[2], (int)ahi[3]};
+      y = mfma_fp8(af, wf, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+    if constexpr (DIAG) {
+      const int col = n0 + r16;
+      #pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int row = 16 * r + 4 * q4 + k;
+        if (row >= p.win_m0 && row < p.win_m1 && col >= p.win_n0 && col < p.win_n1) {
+          const size_t idx = ((size_t)(row - p.win_m0) * (p.win_n1 - p.win_n0) +
+                              (col - p.win_n0)) * NG + g;
+          p.acc[idx] = (int32_t)(y[k] * kUnit);
         }
       }
+    } else {
+      const float sa = __half2float(__ushort_as_half((unsigned short)s.sa[r])) * kUnit;
+      const float sw = __half2float(__ushort_as_half((unsigned short)s.sw));
+      const f32x4 P = scale_products(sa, sw);
+      #pragma unroll
+      for (int k = 0; k < 4; ++k) C[r][k] = __builtin_fmaf(y[k], P[k], C[r][k]);
     }
   }
 }
 
 // Compiler barrier: loads issued before it stay before it, and no
 // instruction of the following compute is scheduled above it.  Without it the
-// compiler sinks each batch's loads down to their first use, which turns the
-// double buffering back into load-then-wait.  It orders only the issue; no
-// wait for the loaded values is implied.
+// compiler sinks loads down to their first use, which turns the prefetching
+// back into load-then-wait.  It orders only the issue; no wait for the loaded
+// values is implied.
 __device__ __forceinline__ void issue_point() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// Schedule positions [pos, end), all of precision B8, in double-buffered
-// batches: the loads of one batch are in flight while the other computes.
-// Loads run at most 2 * kD - 1 positions past `end`.
-template <int R, bool B8, bool DIAG>
-__device__ __forceinline__ void stream(const GemmArgs& p, int pos, int end, int col, int n0,
-                                       f32x4 (&C)[R]) {
-  if (pos >= end) return;
-  Batch<R, B8> x, y;
-  load_batch<R, B8>(p, pos, col, x);
-  for (;;) {
-    load_batch<R, B8>(p, pos + kD, col, y);
+// One batch: K-blocks gb .. gb + 3 (those below g1 are computed) from weights
+// `wc`, while the next batch's weights load into `wn`.  The activation step
+// of K-block gb is in `x` on entry; `x` and `y` alternate, and the step of
+// K-block gb + 4 is in `x` on exit.
+template <int R, bool DIAG>
+__device__ __forceinline__ void batch(const GemmArgs& p, uint8_t* wbuf, int gb, int g1, int n0,
+                                      int col, int& aoff, const u32x4 (&wc)[4], u32x4 (&wn)[4],
+                                      AStep<R>& x, AStep<R>& y, f32x4 (&C)[R]) {
+  const int NG = p.K / kG;
+  load_w(p, gb + kD, n0, wn);
+  store_w(wbuf, wc);
+  #pragma unroll
+  for (int i = 0; i < kD; ++i) {
+    const int g = gb + i;
+    const bool b8 = is8(p, min(g, NG - 1));
+    // next step's activations: K-block g + 1 (clamped into range)
+    const int gn = min(g + 1, NG - 1);
+    const int an = g + 1 < NG ? aoff + 1 + (b8 ? 1 : 0) : aoff;
+    AStep<R>& cur = (i & 1) ? y : x;
+    AStep<R>& nxt = (i & 1) ? x : y;
+    load_a<R>(p, gn, an, col, nxt);
     issue_point();
-    compute_batch<R, B8, DIAG>(p, pos, end, n0, x, C);
-    if (pos + kD >= end) break;
-    load_batch<R, B8>(p, pos + 2 * kD, col, x);
-    issue_point();
-    compute_batch<R, B8, DIAG>(p, pos + kD, end, n0, y, C);
-    pos += 2 * kD;
-    if (pos >= end) break;
+    if (g < g1) compute_step<R, DIAG>(p, wbuf, i, g, b8, n0, cur, C);
+    aoff = an;
   }
 }
 
@@ -178,28 +209,39 @@ __device__ __forceinline__ void stream(const GemmArgs& p, int pos, int end, int 
 // L2: measured ~12x slower for a 70B-sized weight stream.)
 template <int R, bool DIAG>
 __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
+  __shared__ __attribute__((aligned(16))) uint8_t wlds[kWaves][16 * 256];
   __shared__ f32x4 red[kWaves][R][64];
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, q4 = lane >> 4;
   const int S = p.splits;
-  // wave-uniform indices (readfirstlane keeps the schedule walk in scalar
-  // registers)
+  // wave-uniform indices (readfirstlane keeps the walk in scalar registers)
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int cb = blockIdx.x * (kWaves / S) + wave / S, slot = wave % S;
   const bool active = cb < p.N / 16;  // the last workgroup may be partly idle
-  const int n0 = cb * 16;
+  const int n0 = active ? cb * 16 : 0;
   const int col = n0 + r16;
   const int NG = p.K / kG;
-  // this slot's share of the schedule positions
+  // this slot's K-blocks, in natural order
   const int g0 = NG * slot / S, g1 = NG * (slot + 1) / S;
-  const int split = min(max(p.n4, g0), g1);
 
   f32x4 C[R];
   #pragma unroll
   for (int r = 0; r < R; ++r) C[r] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (active) {
-    stream<R, false, DIAG>(p, g0, split, col, n0, C);
-    stream<R, true, DIAG>(p, split, g1, col, n0, C);
+  if (active && g0 < g1) {
+    uint8_t* wbuf = wlds[wave];
+    u32x4 wa[4], wb[4];
+    AStep<R> x, y;
+    int aoff = aoff_of(p, g0);
+    load_w(p, g0, n0, wa);
+    load_a<R>(p, g0, aoff, col, x);
+    for (int gb = g0;;) {
+      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wa, wb, x, y, C);
+      gb += kD;
+      if (gb >= g1) break;
+      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wb, wa, x, y, C);
+      gb += kD;
+      if (gb >= g1) break;
+    }
   }
   if constexpr (DIAG) return;
 
