@@ -304,7 +304,8 @@ def cpu_baseline(layers, rows_per_layer: int) -> dict:
     return {
         "value": round(ops / t_total / 1e12, 5), "unit": "TOPS", "cores": threads,
         "kind": "oracle", "seconds": round(t_total, 2),
-        "sample": f"first {rows_per_layer} token rows of each layer (quantize + fp64-dequant GEMM)",
+        "sample": ", ".join(f"{L['name']}: first {min(rows_per_layer, L['M'])} of {L['M']} token rows"
+                            for L in layers) + " (quantize + fp64-dequant GEMM)",
         "parity_max_rel": worst, "parity_norm_rel": worst_norm, "parity_ok": worst <= 2e-3,
     }
 
