@@ -40,7 +40,15 @@ constexpr int kWaves = 4;  // waves per workgroup; the split-K slot count divide
 template <int R>
 struct AStep {
   u32x4 a[R][2];
-  uint32_t sa[R];  // raw fp16 bits, converted when used
+};
+
+// Scales of one batch, one load per row block (activations) and one for the
+// weights: lane l holds the activation scale of row 16 r + l % 16 and the
+// weight scale of column n0 + l % 16, both of K-block gb + l / 16.  A step
+// takes its values from the lanes of its K-block (cross-lane reads).
+template <int R>
+struct SBatch {
+  uint32_t sa[R];
   uint32_t sw;
 };
 
@@ -72,11 +80,18 @@ __device__ __forceinline__ void load_a(const GemmArgs& p, int g, int aoff, int c
     const uint8_t* base = A + (row << (6 + b8)) + ((uint32_t)q4 << (4 + b8));
     s.a[r][0] = *reinterpret_cast<const u32x4*>(base);
     s.a[r][1] = *reinterpret_cast<const u32x4*>(base + (b8 << 4));
-    // 4x4x1 operand: activation scale of row 16 r + 4 q4 + (lane & 3)
-    const int srow = min(16 * r + 4 * q4 + (lane & 3), p.M - 1);
-    s.sa[r] = p.sa[(size_t)g * p.M + srow];
   }
-  s.sw = p.sw[(size_t)g * p.N + col];
+  (void)col;
+}
+
+template <int R>
+__device__ __forceinline__ void load_scales(const GemmArgs& p, int gb, int n0, SBatch<R>& s) {
+  const int lane = threadIdx.x & 63;
+  const int g = min(gb + (lane >> 4), p.K / kG - 1);
+  #pragma unroll
+  for (int r = 0; r < R; ++r)
+    s.sa[r] = p.sa[(size_t)g * p.M + min(16 * r + (lane & 15), p.M - 1)];
+  s.sw = p.sw[(size_t)g * p.N + n0 + (lane & 15)];
 }
 
 // Weights of the batch starting at K-block gb for the wave's 16 rows n0..:
@@ -113,7 +128,7 @@ __device__ __forceinline__ void store_w(uint8_t* buf, const u32x4 (&w)[4]) {
 template <int R, bool DIAG>
 __device__ __forceinline__ void compute_step(const GemmArgs& p, const uint8_t* wbuf, int i,
                                              int g, bool b8, int n0, const AStep<R>& s,
-                                             f32x4 (&C)[R]) {
+                                             const SBatch<R>& sc, f32x4 (&C)[R]) {
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, q4 = lane >> 4;
   const int NG = p.K / kG;
@@ -155,8 +170,12 @@ __device__ __forceinline__ void compute_step(const GemmArgs& p, const uint8_t* w
         }
       }
     } else {
-      const float sa = __half2float(__ushort_as_half((unsigned short)s.sa[r])) * kUnit;
-      const float sw = __half2float(__ushort_as_half((unsigned short)s.sw));
+      // 4x4x1 operands: activation scale of row 16 r + 4 q4 + (lane & 3),
+      // weight scale of column n0 + lane % 16
+      const uint32_t sab = (uint32_t)__shfl((int)sc.sa[r], 16 * i + 4 * q4 + (lane & 3));
+      const uint32_t swb = (uint32_t)__shfl((int)sc.sw, 16 * i + r16);
+      const float sa = __half2float(__ushort_as_half((unsigned short)sab)) * kUnit;
+      const float sw = __half2float(__ushort_as_half((unsigned short)swb));
       const f32x4 P = scale_products(sa, sw);
       #pragma unroll
       for (int k = 0; k < 4; ++k) C[r][k] = __builtin_fmaf(y[k], P[k], C[r][k]);
@@ -181,9 +200,11 @@ __device__ __forceinline__ void issue_point() {
 template <int R, bool DIAG>
 __device__ __forceinline__ void batch(const GemmArgs& p, uint8_t* wbuf, int gb, int g1, int n0,
                                       int col, int& aoff, const u32x4 (&wc)[4], u32x4 (&wn)[4],
-                                      AStep<R>& x, AStep<R>& y, f32x4 (&C)[R]) {
+                                      const SBatch<R>& sc, SBatch<R>& sn, AStep<R>& x,
+                                      AStep<R>& y, f32x4 (&C)[R]) {
   const int NG = p.K / kG;
   load_w(p, gb + kD, n0, wn);
+  load_scales<R>(p, gb + kD, n0, sn);
   store_w(wbuf, wc);
   #pragma unroll
   for (int i = 0; i < kD; ++i) {
@@ -196,7 +217,7 @@ __device__ __forceinline__ void batch(const GemmArgs& p, uint8_t* wbuf, int gb, 
     AStep<R>& nxt = (i & 1) ? x : y;
     load_a<R>(p, gn, an, col, nxt);
     issue_point();
-    if (g < g1) compute_step<R, DIAG>(p, wbuf, i, g, b8, n0, cur, C);
+    if (g < g1) compute_step<R, DIAG>(p, wbuf, i, g, b8, n0, cur, sc, C);
     aoff = an;
   }
 }
@@ -230,15 +251,17 @@ __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
   if (active && g0 < g1) {
     uint8_t* wbuf = wlds[wave];
     u32x4 wa[4], wb[4];
+    SBatch<R> sa_, sb_;
     AStep<R> x, y;
     int aoff = aoff_of(p, g0);
     load_w(p, g0, n0, wa);
+    load_scales<R>(p, g0, n0, sa_);
     load_a<R>(p, g0, aoff, col, x);
     for (int gb = g0;;) {
-      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wa, wb, x, y, C);
+      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wa, wb, sa_, sb_, x, y, C);
       gb += kD;
       if (gb >= g1) break;
-      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wb, wa, x, y, C);
+      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wb, wa, sb_, sa_, x, y, C);
       gb += kD;
       if (gb >= g1) break;
     }
