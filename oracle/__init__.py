@@ -45,6 +45,11 @@ def _load():
         "orc_group_acc": (None, [P, P, I, I, I, I, P]),
         "orc_dequant_gemm": (None, [P, P, P, P, I, I, I, I, P, I, P, I]),
         "orc_exact_gemm": (None, [P, P, I, I, I, P, I]),
+        "orc_permute_columns": (I, [P, P, I, I, P]),
+        "orc_channel_absmax": (None, [P, I, I, P]),
+        "orc_plan_channel_perm": (I, [P, I, I, ctypes.c_float, ctypes.c_float, P, P, P]),
+        "orc_kv4_quantize": (I, [P, I, I, I, P, P]),
+        "orc_kv4_dequantize": (I, [P, P, I, I, I, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -197,4 +202,64 @@ def exact_gemm(X16, W16, nthreads: int = 0) -> np.ndarray:
     N = W16.shape[0]
     out = np.empty((M, N), dtype=np.float64)
     _load().orc_exact_gemm(_p(X16), _p(W16), M, N, K, _p(out), nthreads)
+    return out
+
+
+# --- channel permutation and calibration map (Sec. 3.2) ---------------------------
+
+def permute_columns(X16, perm) -> np.ndarray:
+    """out[r][c] = X16[r][perm[c]] (uint16 fp16 bits)."""
+    X16 = _c(X16, np.uint16)
+    perm = _c(perm, np.int32)
+    R, K = X16.shape
+    out = np.empty((R, K), dtype=np.uint16)
+    if _load().orc_permute_columns(_p(X16), _p(perm), R, K, _p(out)):
+        raise ValueError("permutation index out of range")
+    return out
+
+
+def channel_absmax(X16, absmax=None) -> np.ndarray:
+    """fp32 [K] running maximum of |X| per channel over the rows of X16."""
+    X16 = _c(X16, np.uint16)
+    M, K = X16.shape
+    out = np.zeros(K, np.float32) if absmax is None else _c(absmax, np.float32).copy()
+    _load().orc_channel_absmax(_p(X16), M, K, _p(out))
+    return out
+
+
+def plan_channel_perm(absmax, G: int, outlier_ratio: float, max_frac8: float):
+    """Returns (perm int32 [K], prec uint8 [K/G], n_outliers)."""
+    a = _c(absmax, np.float32).reshape(-1)
+    K = a.size
+    perm = np.empty(K, np.int32)
+    prec = np.empty(K // G if G > 0 else 0, np.uint8)
+    nout = np.zeros(1, np.int32)
+    rc = _load().orc_plan_channel_perm(_p(a), K, G, outlier_ratio, max_frac8, _p(perm), _p(prec),
+                                       _p(nout))
+    if rc:
+        raise ValueError("oracle rejected the calibration arguments")
+    return perm, prec, int(nout[0])
+
+
+# --- KV4 ------------------------------------------------------------------------------
+
+def kv4_quantize(X16, G: int = 128):
+    """X16 uint16 [T][C] -> (codes uint8 [T][C/2], params uint16 [T][C/G][2])."""
+    X16 = _c(X16, np.uint16)
+    T, C = X16.shape
+    codes = np.empty((T, C // 2), np.uint8)
+    params = np.empty((T, C // G, 2), np.uint16)
+    if _load().orc_kv4_quantize(_p(X16), T, C, G, _p(codes), _p(params)):
+        raise ValueError("oracle rejected the KV rows")
+    return codes, params
+
+
+def kv4_dequantize(codes, params, G: int = 128) -> np.ndarray:
+    codes = _c(codes, np.uint8)
+    params = _c(params, np.uint16)
+    T = codes.shape[0]
+    C = codes.shape[1] * 2
+    out = np.empty((T, C), np.uint16)
+    if _load().orc_kv4_dequantize(_p(codes), _p(params), T, C, G, _p(out)):
+        raise ValueError("bad arguments to kv4_dequantize")
     return out

@@ -10,6 +10,7 @@
 #include "oracle.h"
 
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #ifdef _OPENMP
@@ -267,4 +268,164 @@ void orc_exact_gemm(const uint16_t* X, const uint16_t* W, int M, int N, int K, d
              (double)orc_f32_from_f16(W[(size_t)n * K + k]);
       exact[(size_t)m * N + n] = s;
     }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Channel permutation and the calibration map (Sec. 3.2).  Outlier channels  */
+/* are found from sampled activations and gathered into a few blocks, which   */
+/* are the ones quantized to 8 bits; the weight columns take the same         */
+/* permutation, so X W^T is unchanged.                                        */
+/* ------------------------------------------------------------------------- */
+
+int orc_permute_columns(const uint16_t* X, const int32_t* perm, int R, int K, uint16_t* out) {
+  if (R < 0 || K <= 0) return -1;
+  for (int c = 0; c < K; ++c)
+    if (perm[c] < 0 || perm[c] >= K) return -1;
+  for (int r = 0; r < R; ++r)
+    for (int c = 0; c < K; ++c) out[(size_t)r * K + c] = X[(size_t)r * K + perm[c]];
+  return 0;
+}
+
+void orc_channel_absmax(const uint16_t* X, int M, int K, float* absmax) {
+  for (int m = 0; m < M; ++m)
+    for (int c = 0; c < K; ++c) {
+      float a = fabsf(orc_f32_from_f16(X[(size_t)m * K + c]));
+      if (a > absmax[c]) absmax[c] = a;
+    }
+}
+
+static int cmp_float_asc(const void* a, const void* b) {
+  float x = *(const float*)a, y = *(const float*)b;
+  return (x > y) - (x < y);
+}
+
+/* Ranking order: larger absmax first, equal values by smaller channel index. */
+static const float* g_rank_key;
+static int cmp_rank(const void* a, const void* b) {
+  int i = *(const int32_t*)a, j = *(const int32_t*)b;
+  float x = g_rank_key[i], y = g_rank_key[j];
+  if (x != y) return x > y ? -1 : 1;
+  return (i > j) - (i < j);
+}
+
+int orc_plan_channel_perm(const float* absmax, int K, int G, float outlier_ratio,
+                          float max_frac8, int32_t* perm, uint8_t* prec, int* n_outliers) {
+  if (K <= 0 || G <= 0 || K % G) return -1;
+  if (!(max_frac8 >= 0.0f && max_frac8 <= 1.0f) || isnan(outlier_ratio)) return -1;
+  for (int c = 0; c < K; ++c)
+    if (!(absmax[c] >= 0.0f) || isinf(absmax[c])) return -1;
+  const int NG = K / G;
+
+  /* Lower median of the per-channel maxima. */
+  float* sorted = (float*)malloc(sizeof(float) * (size_t)K);
+  int32_t* rank = (int32_t*)malloc(sizeof(int32_t) * (size_t)K);
+  unsigned char* taken = (unsigned char*)calloc((size_t)K, 1);
+  if (!sorted || !rank || !taken) {
+    free(sorted);
+    free(rank);
+    free(taken);
+    return -1;
+  }
+  memcpy(sorted, absmax, sizeof(float) * (size_t)K);
+  qsort(sorted, (size_t)K, sizeof(float), cmp_float_asc);
+  double median = (double)sorted[(K - 1) / 2];
+
+  /* Outlier channels: maxima above ratio x median (every channel if ratio <= 0). */
+  int nout = 0;
+  if (outlier_ratio <= 0.0f) {
+    nout = K;
+  } else {
+    double thr = (double)outlier_ratio * median;
+    for (int c = 0; c < K; ++c)
+      if ((double)absmax[c] > thr) ++nout;
+  }
+
+  /* 8-bit blocks: enough to hold every outlier, at most a fraction of all blocks. */
+  int need = (nout + G - 1) / G;
+  int cap = (int)floor((double)max_frac8 * (double)NG);
+  int n8 = need < cap ? need : cap;
+
+  /* The n8*G highest-ranked channels fill the 8-bit blocks in rank order; the
+   * rest follow in their original order. */
+  for (int c = 0; c < K; ++c) rank[c] = c;
+  g_rank_key = absmax;
+  qsort(rank, (size_t)K, sizeof(int32_t), cmp_rank);
+  int pos = 0;
+  for (int i = 0; i < n8 * G; ++i) {
+    perm[pos++] = rank[i];
+    taken[rank[i]] = 1;
+  }
+  for (int c = 0; c < K; ++c)
+    if (!taken[c]) perm[pos++] = c;
+  for (int g = 0; g < NG; ++g) prec[g] = g < n8 ? 8 : 4;
+  if (n_outliers) *n_outliers = nout;
+  free(sorted);
+  free(rank);
+  free(taken);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* KV4: asymmetric 4-bit group quantization of the KV cache (Sec. 3.2, and    */
+/* the setup of Sec. 6).  A group is G consecutive channels of one token's K  */
+/* or V vector.  Per group: mn = min x, s = fp16(fp32(max x - mn) / 15),      */
+/* q = clamp(rint(fp32(fp32(x - mn) / s)), 0, 15) (q = 0 when s == 0);        */
+/* reconstruction x' = fp16(fp32(fp32(q * s) + mn)).                          */
+/* codes: [T][C/2] bytes, channel 2j in the low nibble of byte j, 2j+1 in the */
+/* high nibble; params: fp16 [T][C/G][2] = {s, mn}.                           */
+/* ------------------------------------------------------------------------- */
+
+int orc_kv4_quantize(const uint16_t* X, int T, int C, int G, uint8_t* codes, uint16_t* params) {
+  if (T < 0 || C <= 0 || G <= 0 || G % 2 || C % G) return -1;
+  const int NG = C / G;
+  for (int t = 0; t < T; ++t)
+    for (int g = 0; g < NG; ++g) {
+      const uint16_t* x16 = X + (size_t)t * C + (size_t)g * G;
+      float mn = orc_f32_from_f16(x16[0]), mx = mn;
+      for (int c = 0; c < G; ++c) {
+        float v = orc_f32_from_f16(x16[c]);
+        if (!isfinite(v)) return -1;
+        if (v < mn) mn = v;
+        if (v > mx) mx = v;
+      }
+      float range = mx - mn;
+      uint16_t s16 = orc_f16_from_f32(range / 15.0f);
+      float s = orc_f32_from_f16(s16);
+      uint8_t* out = codes + (size_t)t * (C / 2) + (size_t)g * (G / 2);
+      for (int c = 0; c < G; c += 2) {
+        unsigned q2[2];
+        for (int i = 0; i < 2; ++i) {
+          float r = 0.0f;
+          if (s != 0.0f) {
+            float d = orc_f32_from_f16(x16[c + i]) - mn;
+            r = rintf(d / s);
+            if (r > 15.0f) r = 15.0f;
+            if (r < 0.0f) r = 0.0f;
+          }
+          q2[i] = (unsigned)r;
+        }
+        out[c / 2] = (uint8_t)(q2[0] | (q2[1] << 4));
+      }
+      uint16_t* p = params + ((size_t)t * NG + g) * 2;
+      p[0] = s16;
+      p[1] = orc_f16_from_f32(mn); /* mn is an input value: exact in fp16 */
+    }
+  return 0;
+}
+
+int orc_kv4_dequantize(const uint8_t* codes, const uint16_t* params, int T, int C, int G,
+                       uint16_t* out) {
+  if (T < 0 || C <= 0 || G <= 0 || G % 2 || C % G) return -1;
+  const int NG = C / G;
+  for (int t = 0; t < T; ++t)
+    for (int c = 0; c < C; ++c) {
+      const uint16_t* p = params + ((size_t)t * NG + c / G) * 2;
+      float s = orc_f32_from_f16(p[0]);
+      float mn = orc_f32_from_f16(p[1]);
+      uint8_t b = codes[(size_t)t * (C / 2) + c / 2];
+      unsigned q = (c & 1) ? (unsigned)(b >> 4) : (unsigned)(b & 15);
+      float prod = (float)q * s;
+      out[(size_t)t * C + c] = orc_f16_from_f32(prod + mn);
+    }
+  return 0;
 }

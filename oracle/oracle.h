@@ -86,6 +86,35 @@ void orc_dequant_gemm(const int8_t* qa, const uint16_t* sa16, const int8_t* qw,
 void orc_exact_gemm(const uint16_t* X, const uint16_t* W, int M, int N, int K, double* exact,
                     int nthreads);
 
+/* Channel permutation and calibration map (Sec. 3.2).
+ * orc_permute_columns: out[r][c] = X[r][perm[c]] for R rows of K fp16 values;
+ *   -1 if an index is outside [0, K).
+ * orc_channel_absmax: absmax[c] = max(absmax[c], max_m |X[m][c]|) (fp32,
+ *   accumulating over calls; start from zeros).
+ * orc_plan_channel_perm: from per-channel maxima, the lower median med (rank
+ *   (K-1)/2 ascending) gives the outlier channels, absmax > ratio * med
+ *   (compared in fp64; every channel if ratio <= 0).  The number of 8-bit
+ *   blocks is n8 = min(ceil(n_out / G), floor(max_frac8 * K/G)).  Channels are
+ *   ranked by absmax descending, ties by index; perm[0 .. n8*G) holds the first
+ *   n8*G ranked channels in rank order and perm[n8*G .. K) the rest in
+ *   ascending order; prec[g] = 8 for g < n8, else 4.  Returns 0, or -1 for bad
+ *   arguments (max_frac8 outside [0, 1], a negative or non-finite maximum). */
+int orc_permute_columns(const uint16_t* X, const int32_t* perm, int R, int K, uint16_t* out);
+void orc_channel_absmax(const uint16_t* X, int M, int K, float* absmax);
+int orc_plan_channel_perm(const float* absmax, int K, int G, float outlier_ratio,
+                          float max_frac8, int32_t* perm, uint8_t* prec, int* n_outliers);
+
+/* KV4: asymmetric 4-bit group quantization of K/V rows (Sec. 3.2; Sec. 6 setup).
+ * X fp16 [T][C], groups of G consecutive channels (G even, C % G == 0).
+ *   mn = min, s = fp16(fp32(max - mn) / 15), q = clamp(rint(fp32(fp32(x - mn) / s)), 0, 15)
+ *   (all zero when s == 0).  codes [T][C/2]: channel 2j low nibble of byte j,
+ *   2j+1 high nibble.  params fp16 [T][C/G][2] = {s, mn}.
+ * Dequantization: x' = fp16(fp32(q * s) + mn).  Return 0, or -1 for bad
+ * arguments or a non-finite input. */
+int orc_kv4_quantize(const uint16_t* X, int T, int C, int G, uint8_t* codes, uint16_t* params);
+int orc_kv4_dequantize(const uint8_t* codes, const uint16_t* params, int T, int C, int G,
+                       uint16_t* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,7 +15,13 @@ Workload recipe (synthetic LLaMA-shaped layers):
     multiplied by 50 before rounding (outlier channels);
   * weights W [N][K] ~ N(0, 0.02^2);
   * block precision map: a contiguous run of 8-bit blocks starting at block
-    floor(3 * NG / 8), or a seeded random subset of blocks.
+    floor(3 * NG / 8), or a seeded random subset of blocks;
+  * calibration workloads (channel permutation): ``n_out`` outlier channels
+    scattered over all K channels (a seeded subset), multiplied by 50; with
+    n_out = 0.5% of K this matches "a small cluster, usually under 1% of the
+    features" for LLaMA-scale models;
+  * KV rows [T][C] (C = KV heads x head_dim) ~ N(0, 1) with per-channel
+    multipliers drawn from 2^U(0, 3), so channels differ in range.
 """
 from __future__ import annotations
 
@@ -31,6 +37,10 @@ _M2 = np.uint64(0x94D049BB133111EB)
 TID_X = 1
 TID_W = 2
 TID_MAP = 3
+TID_OUTLIER = 4
+TID_CAL = 5
+TID_KV = 6
+TID_KV_SCALE = 7
 
 _CHUNK = 1 << 22
 
@@ -108,9 +118,7 @@ def prec_map(NG: int, n8: int, placement: str = "contiguous", seed: int = 0,
         for j in range(n8):
             m[(s + j) % NG] = 8
     elif placement == "random":
-        key = _key(seed, TID_MAP)
-        with np.errstate(over="ignore"):
-            words = mix64(key + (np.arange(NG, dtype=np.uint64) + np.uint64(1)) * GOLDEN)
+        words = _words(seed, TID_MAP, NG)
         idx = list(range(NG))
         for i in range(NG - 1, 0, -1):
             j = int(words[i] % np.uint64(i + 1))
@@ -119,6 +127,42 @@ def prec_map(NG: int, n8: int, placement: str = "contiguous", seed: int = 0,
     else:
         raise ValueError(placement)
     return m
+
+
+def _words(seed: int, tid: int, n: int) -> np.ndarray:
+    key = _key(seed, tid)
+    with np.errstate(over="ignore"):
+        return mix64(key + (np.arange(n, dtype=np.uint64) + np.uint64(1)) * GOLDEN)
+
+
+def outlier_channels(K: int, n_out: int, seed: int = 0) -> np.ndarray:
+    """Sorted int64 array of ``n_out`` distinct channels, a seeded Fisher-Yates subset."""
+    words = _words(seed, TID_OUTLIER, K)
+    idx = list(range(K))
+    for i in range(K - 1, 0, -1):
+        j = int(words[i] % np.uint64(i + 1))
+        idx[i], idx[j] = idx[j], idx[i]
+    return np.sort(np.array(idx[:n_out], dtype=np.int64))
+
+
+def channel_scale(K: int, channels, factor: float = 50.0) -> np.ndarray:
+    """Per-channel multiplier: ``factor`` on ``channels``, else 1."""
+    cs = np.ones(K, dtype=np.float64)
+    cs[np.asarray(channels, dtype=np.int64)] = factor
+    return cs
+
+
+def calibration_activations(seed: int, M: int, K: int, channels, tid: int = TID_CAL,
+                            factor: float = 50.0) -> np.ndarray:
+    """Activations with outliers on the given (scattered) channels."""
+    return normal_fp16(seed, tid, (M, K), 1.0, channel_scale(K, channels, factor))
+
+
+def kv_rows(seed: int, T: int, C: int) -> np.ndarray:
+    """K or V rows [T][C] with per-channel ranges 2^U(0, 3)."""
+    w = _words(seed, TID_KV_SCALE, C)
+    u = (w >> np.uint64(11)).astype(np.float64) * (1.0 / 9007199254740992.0)
+    return normal_fp16(seed, TID_KV, (T, C), 1.0, np.exp2(3.0 * u))
 
 
 def outlier_scale(prec: np.ndarray, G: int = 128, factor: float = 50.0) -> np.ndarray:
