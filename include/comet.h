@@ -101,6 +101,75 @@ COMET_API comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_
 COMET_API comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
                              int K, int G, hipStream_t stream);
 
+/* Channel permutation (Sec. 3.2): outlier channels are gathered into a few
+ * blocks so that only those need 8 bits; the weight columns take the same
+ * permutation, so out = X W^T is unchanged up to quantization.
+ *
+ * Same as comet_fmpq_quantize_act, on the permuted activations: block g of
+ * row m quantizes X[m][perm[gG + c]], c < G.  perm is a DEVICE int32 [K]
+ * array, 16-byte aligned, normally a permutation of 0..K-1 (repeated entries
+ * are gathered as written; an entry outside [0, K), negative ones included,
+ * reads channel K-1, so no read leaves the row).  perm == NULL: no
+ * permutation (identical to comet_fmpq_quantize_act).  Other arguments and
+ * errors as there. */
+COMET_API comet_status_t comet_fmpq_quantize_act_perm(const uint16_t* X, const int32_t* perm,
+                                                      const uint8_t* group_prec_map,
+                                                      uint8_t* A_packed, uint16_t* a_scales,
+                                                      int M, int K, int G, hipStream_t stream);
+
+/* comet_pack_w4 on the column-permuted weights W[n][perm[k]] (Sec. 3.2, the
+ * matching permutation of the weight matrix).  perm as above; NULL = none. */
+COMET_API comet_status_t comet_pack_w4_perm(const uint16_t* W, const int32_t* perm,
+                                            uint8_t* W_packed, uint16_t* w_scales, int N, int K,
+                                            int G, hipStream_t stream);
+
+/* Data sampling for the calibration (Sec. 3.2): absmax[c] = max(absmax[c],
+ * max_m |X[m][c]|) over the M rows of X (device, fp16 [M][K], 16-byte
+ * aligned, K a multiple of 8).  absmax is a device fp32 [K] array, 4-byte
+ * aligned, that the call ACCUMULATES into: start it at zeros and call once
+ * per calibration batch.  It must hold non-negative values (the merge is an
+ * unsigned compare of the bit patterns).  Bit-exact: max is order-free.
+ * Non-finite inputs are not supported. */
+COMET_API comet_status_t comet_channel_absmax(const uint16_t* X, float* absmax, int M, int K,
+                                              hipStream_t stream);
+
+/* Host-only calibration map (Sec. 3.2; nothing is launched).  From the
+ * per-channel maxima absmax[K] (host), with med the lower median (rank
+ * (K-1)/2 ascending):
+ *   outlier channels: absmax > outlier_ratio * med, compared in fp64
+ *                     (every channel when outlier_ratio <= 0);
+ *   n8 = min(ceil(n_out / G), floor(max_frac_8bit * K/G)) 8-bit blocks;
+ *   perm (host int32 [K]): the n8*G channels with the largest maxima (ties by
+ *        index) in that order, then every other channel in ascending order;
+ *   group_prec_map (host uint8 [K/G]): 8 for g < n8, else 4;
+ *   *n_outliers (may be NULL): n_out.
+ * G is any positive divisor of K here (the GEMM needs 128).  Errors:
+ * COMET_ERR_INVALID_ARG for null pointers, K % G != 0, max_frac_8bit outside
+ * [0, 1], a NaN ratio or a negative / non-finite maximum. */
+COMET_API comet_status_t comet_plan_channel_perm(const float* absmax, int K, int G,
+                                                 float outlier_ratio, float max_frac_8bit,
+                                                 int32_t* perm, uint8_t* group_prec_map,
+                                                 int* n_outliers);
+
+/* KV4: 4-bit asymmetric group quantization of K/V cache rows (Sec. 3.2: the
+ * KV cache is quantized to 4 bits channel-wise; Sec. 6 setup: asymmetric
+ * INT4 groups).  X: device fp16 [T][C] (C = KV heads x head_dim), 16-byte
+ * aligned; groups of G in {32, 64, 128} consecutive channels, C % G == 0.
+ * Per group: mn = min x, mx = max x (zero extremes as +0), s = fp16(fp32(mx - mn) / 15),
+ * q = clamp(rint(fp32(fp32(x - mn) / s)), 0, 15) (all 0 when s == 0).
+ *   codes  device [T][C/2] bytes, 4-byte aligned: channel 2j in the low
+ *          nibble of byte j, 2j+1 in the high nibble;
+ *   params device fp16 [T][C/G][2] = {s, mn}, 4-byte aligned.
+ * Bit-exact with the definition above.  Non-finite inputs are not supported. */
+COMET_API comet_status_t comet_kv4_quantize(const uint16_t* X, uint8_t* codes, uint16_t* params,
+                                            int T, int C, int G, hipStream_t stream);
+
+/* Inverse of comet_kv4_quantize: out[t][c] = fp16(fp32(q * s) + mn) (device
+ * fp16 [T][C], 16-byte aligned); the other arguments as there. */
+COMET_API comet_status_t comet_kv4_dequantize(const uint8_t* codes, const uint16_t* params,
+                                              uint16_t* out, int T, int C, int G,
+                                              hipStream_t stream);
+
 /* W4Ax GEMM (Sec. 4, O = WX): out[m][n] = fp16( sum_g a_scales[g][m] *
  * w_scales[g][n] * sum_{c<G} qa[m][gG+c] * qw[n][gG+c] ).  The per-block sums
  * are exact; the sum over blocks is fp32 in an unspecified order, rounded once

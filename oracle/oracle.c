@@ -388,6 +388,10 @@ int orc_kv4_quantize(const uint16_t* X, int T, int C, int G, uint8_t* codes, uin
         if (v < mn) mn = v;
         if (v > mx) mx = v;
       }
+      /* zero extremes as +0, whatever the signs of the zeros (min and max of
+       * +0 and -0 are value ties) */
+      if (mn == 0.0f) mn = 0.0f;
+      if (mx == 0.0f) mx = 0.0f;
       float range = mx - mn;
       uint16_t s16 = orc_f16_from_f32(range / 15.0f);
       float s = orc_f32_from_f16(s16);

@@ -106,7 +106,8 @@ int orc_plan_channel_perm(const float* absmax, int K, int G, float outlier_ratio
 
 /* KV4: asymmetric 4-bit group quantization of K/V rows (Sec. 3.2; Sec. 6 setup).
  * X fp16 [T][C], groups of G consecutive channels (G even, C % G == 0).
- *   mn = min, s = fp16(fp32(max - mn) / 15), q = clamp(rint(fp32(fp32(x - mn) / s)), 0, 15)
+ *   mn = min, mx = max (zero extremes as +0), s = fp16(fp32(mx - mn) / 15),
+ *   q = clamp(rint(fp32(fp32(x - mn) / s)), 0, 15)
  *   (all zero when s == 0).  codes [T][C/2]: channel 2j low nibble of byte j,
  *   2j+1 high nibble.  params fp16 [T][C/G][2] = {s, mn}.
  * Dequantization: x' = fp16(fp32(q * s) + mn).  Return 0, or -1 for bad

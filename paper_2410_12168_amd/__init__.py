@@ -6,8 +6,9 @@ runs in libcomet's gfx950 kernels.  PyTorch only provides device memory and
 streams.  There is no CPU fallback: if libcomet.so is missing and cannot be
 built, importing a function raises.
 
-Convenience wrappers (``quantize_act``, ``pack_w4``, ``w4ax_gemm``) allocate
-the outputs with ``torch.empty`` and call the same entry points.
+Convenience wrappers (``quantize_act``, ``pack_w4``, ``w4ax_gemm``,
+``channel_absmax``, ``plan_channel_perm``, ``kv4_quantize``, ``kv4_dequantize``)
+allocate the outputs with ``torch.empty`` and call the same entry points.
 """
 from __future__ import annotations
 
@@ -53,6 +54,12 @@ def lib():
         "comet_w4ax_gemm": (I, [P, P, P, P, P, P, I, I, I, I, P]),
         "comet_w4ax_gemm_acc": (I, [P, P, P, P, P, P, I, I, I, I, I, I, I, I, P]),
         "comet_schedule_query": (I, [I, I, I, I, P, I, P, I, P, P, I, P, P, P, P]),
+        "comet_fmpq_quantize_act_perm": (I, [P, P, P, P, P, I, I, I, P]),
+        "comet_pack_w4_perm": (I, [P, P, P, P, I, I, I, P]),
+        "comet_channel_absmax": (I, [P, P, I, I, P]),
+        "comet_plan_channel_perm": (I, [P, I, I, ctypes.c_float, ctypes.c_float, P, P, P]),
+        "comet_kv4_quantize": (I, [P, P, P, I, I, I, P]),
+        "comet_kv4_dequantize": (I, [P, P, P, I, I, I, P]),
         "comet_status_str": (ctypes.c_char_p, [I]),
         "comet_last_error": (ctypes.c_char_p, []),
         "comet_release_caches": (None, []),
@@ -114,6 +121,40 @@ def comet_pack_w4(W, W_packed, w_scales, N: int, K: int, G: int = G, stream=None
                                _stream(stream)))
 
 
+def comet_fmpq_quantize_act_perm(X, perm, group_prec_map, A_packed, a_scales, M: int, K: int,
+                                 G: int = G, stream=None) -> None:
+    m = _map(group_prec_map)
+    _check(lib().comet_fmpq_quantize_act_perm(_ptr(X), _ptr(perm), _ptr(m), _ptr(A_packed),
+                                              _ptr(a_scales), M, K, G, _stream(stream)))
+
+
+def comet_pack_w4_perm(W, perm, W_packed, w_scales, N: int, K: int, G: int = G,
+                       stream=None) -> None:
+    _check(lib().comet_pack_w4_perm(_ptr(W), _ptr(perm), _ptr(W_packed), _ptr(w_scales), N, K, G,
+                                    _stream(stream)))
+
+
+def comet_channel_absmax(X, absmax, M: int, K: int, stream=None) -> None:
+    _check(lib().comet_channel_absmax(_ptr(X), _ptr(absmax), M, K, _stream(stream)))
+
+
+def comet_plan_channel_perm(absmax, K: int, G: int, outlier_ratio: float, max_frac_8bit: float,
+                            perm, group_prec_map, n_outliers=None) -> None:
+    """Host-only: absmax, perm, group_prec_map (and n_outliers) are host numpy arrays."""
+    _check(lib().comet_plan_channel_perm(_ptr(absmax), K, G, outlier_ratio, max_frac_8bit,
+                                         _ptr(perm), _ptr(group_prec_map), _ptr(n_outliers)))
+
+
+def comet_kv4_quantize(X, codes, params, T: int, C: int, G: int = 128, stream=None) -> None:
+    _check(lib().comet_kv4_quantize(_ptr(X), _ptr(codes), _ptr(params), T, C, G,
+                                    _stream(stream)))
+
+
+def comet_kv4_dequantize(codes, params, out, T: int, C: int, G: int = 128, stream=None) -> None:
+    _check(lib().comet_kv4_dequantize(_ptr(codes), _ptr(params), _ptr(out), T, C, G,
+                                      _stream(stream)))
+
+
 def comet_w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, out, M: int, N: int,
                     K: int, G: int = G, stream=None) -> None:
     m = _map(group_prec_map)
@@ -162,8 +203,9 @@ def comet_release_caches() -> None:
 
 # --- allocating conveniences (torch tensors on the current device) ----------------
 
-def quantize_act(X, group_prec_map, stream=None):
-    """X: float16 [M][K] CUDA tensor -> (A_packed uint8, a_scales float16 [K/G][M])."""
+def quantize_act(X, group_prec_map, perm=None, stream=None):
+    """X: float16 [M][K] CUDA tensor -> (A_packed uint8, a_scales float16 [K/G][M]).
+    perm: optional int32 [K] CUDA tensor (channel permutation)."""
     import torch
 
     M, K = X.shape
@@ -172,19 +214,63 @@ def quantize_act(X, group_prec_map, stream=None):
         raise CometError(1, "invalid map or shape")
     A = torch.empty(nbytes, dtype=torch.uint8, device=X.device)
     sa = torch.empty((K // G, M), dtype=torch.float16, device=X.device)
-    comet_fmpq_quantize_act(X, group_prec_map, A, sa, M, K, G, stream)
+    comet_fmpq_quantize_act_perm(X, perm, group_prec_map, A, sa, M, K, G, stream)
     return A, sa
 
 
-def pack_w4(W, stream=None):
-    """W: float16 [N][K] CUDA tensor -> (W_packed uint8 [N][K/2], w_scales float16 [K/G][N])."""
+def pack_w4(W, perm=None, stream=None):
+    """W: float16 [N][K] CUDA tensor -> (W_packed uint8 [N][K/2], w_scales float16 [K/G][N]).
+    perm: optional int32 [K] CUDA tensor (the activations' channel permutation)."""
     import torch
 
     N, K = W.shape
     Wp = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
     sw = torch.empty((K // G, N), dtype=torch.float16, device=W.device)
-    comet_pack_w4(W, Wp, sw, N, K, G, stream)
+    comet_pack_w4_perm(W, perm, Wp, sw, N, K, G, stream)
     return Wp, sw
+
+
+def channel_absmax(X, absmax=None, stream=None):
+    """Running per-channel max |X| (float32 [K] CUDA tensor), accumulated into absmax."""
+    import torch
+
+    M, K = X.shape
+    if absmax is None:
+        absmax = torch.zeros(K, dtype=torch.float32, device=X.device)
+    comet_channel_absmax(X, absmax, M, K, stream)
+    return absmax
+
+
+def plan_channel_perm(absmax, G: int = G, outlier_ratio: float = 8.0, max_frac_8bit: float = 0.2):
+    """Host: per-channel maxima (numpy or tensor) -> (perm int32 [K], map uint8 [K/G], n_outliers)."""
+    a = np.ascontiguousarray(np.asarray(absmax.cpu() if hasattr(absmax, "cpu") else absmax,
+                                        dtype=np.float32).reshape(-1))
+    K = a.size
+    perm = np.empty(K, np.int32)
+    prec = np.empty(max(K // G, 1), np.uint8)
+    nout = np.zeros(1, np.int32)
+    comet_plan_channel_perm(a, K, G, outlier_ratio, max_frac_8bit, perm, prec, nout)
+    return perm, prec[: K // G], int(nout[0])
+
+
+def kv4_quantize(X, G: int = 128, stream=None):
+    """X: float16 [T][C] CUDA tensor -> (codes uint8 [T][C/2], params float16 [T][C/G][2])."""
+    import torch
+
+    T, C = X.shape
+    codes = torch.empty((T, C // 2), dtype=torch.uint8, device=X.device)
+    params = torch.empty((T, C // G, 2), dtype=torch.float16, device=X.device)
+    comet_kv4_quantize(X, codes, params, T, C, G, stream)
+    return codes, params
+
+
+def kv4_dequantize(codes, params, G: int = 128, stream=None):
+    import torch
+
+    T, C = codes.shape[0], codes.shape[1] * 2
+    out = torch.empty((T, C), dtype=torch.float16, device=codes.device)
+    comet_kv4_dequantize(codes, params, out, T, C, G, stream)
+    return out
 
 
 def w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int, N: int, K: int,

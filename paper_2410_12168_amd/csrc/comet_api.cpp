@@ -345,36 +345,112 @@ size_t comet_act_packed_bytes(const uint8_t* prec, int M, int K, int G) {
   return units * (size_t)M;
 }
 
-comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* prec, uint8_t* A_packed,
-                                       uint16_t* a_scales, int M, int K, int G,
-                                       hipStream_t stream) {
+comet_status_t comet_fmpq_quantize_act_perm(const uint16_t* X, const int32_t* perm,
+                                            const uint8_t* prec, uint8_t* A_packed,
+                                            uint16_t* a_scales, int M, int K, int G,
+                                            hipStream_t stream) {
   if (!X || !A_packed || !a_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
   if (M < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d must be >= 1", M);
   comet_status_t st = check_kg(K, G);
   if (st) return st;
-  if (!aligned16(X) || !aligned16(A_packed) || !aligned16(a_scales))
+  if (!aligned16(X) || !aligned16(A_packed) || !aligned16(a_scales) || !aligned16(perm))
     return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   comet::BlockMap map;
   if ((st = make_map(prec, K / G, &map))) return st;
   int dev;
   DeviceInfo info;
   if ((st = current_device(&dev, &info))) return st;
-  return launched(comet::launch_quantize_act(X, A_packed, a_scales, M, K, map, stream),
+  return launched(comet::launch_quantize_act(X, perm, A_packed, a_scales, M, K, map, stream),
                   "quantize_act launch");
 }
 
-comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
-                             int K, int G, hipStream_t stream) {
+comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* prec, uint8_t* A_packed,
+                                       uint16_t* a_scales, int M, int K, int G,
+                                       hipStream_t stream) {
+  return comet_fmpq_quantize_act_perm(X, nullptr, prec, A_packed, a_scales, M, K, G, stream);
+}
+
+comet_status_t comet_pack_w4_perm(const uint16_t* W, const int32_t* perm, uint8_t* W_packed,
+                                  uint16_t* w_scales, int N, int K, int G, hipStream_t stream) {
   if (!W || !W_packed || !w_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
   if (N < 1) return fail(COMET_ERR_INVALID_ARG, "N=%d must be >= 1", N);
   comet_status_t st = check_kg(K, G);
   if (st) return st;
-  if (!aligned16(W) || !aligned16(W_packed) || !aligned16(w_scales))
+  if (!aligned16(W) || !aligned16(W_packed) || !aligned16(w_scales) || !aligned16(perm))
     return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   int dev;
   DeviceInfo info;
   if ((st = current_device(&dev, &info))) return st;
-  return launched(comet::launch_pack_w4(W, W_packed, w_scales, N, K, stream), "pack_w4 launch");
+  return launched(comet::launch_pack_w4(W, perm, W_packed, w_scales, N, K, stream),
+                  "pack_w4 launch");
+}
+
+comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
+                             int K, int G, hipStream_t stream) {
+  return comet_pack_w4_perm(W, nullptr, W_packed, w_scales, N, K, G, stream);
+}
+
+comet_status_t comet_channel_absmax(const uint16_t* X, float* absmax, int M, int K,
+                                    hipStream_t stream) {
+  if (!X || !absmax) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (M < 1 || K < 8 || K % 8)
+    return fail(COMET_ERR_INVALID_ARG, "M=%d must be >= 1 and K=%d a positive multiple of 8", M,
+                K);
+  if (!aligned16(X) || (reinterpret_cast<uintptr_t>(absmax) & 3u))
+    return fail(COMET_ERR_INVALID_ARG, "X must be 16-byte and absmax 4-byte aligned");
+  comet_status_t st;
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  return launched(comet::launch_channel_absmax(X, absmax, M, K, stream), "channel_absmax launch");
+}
+
+comet_status_t comet_plan_channel_perm(const float* absmax, int K, int G, float outlier_ratio,
+                                       float max_frac_8bit, int32_t* perm,
+                                       uint8_t* group_prec_map, int* n_outliers) {
+  if (!absmax || !perm || !group_prec_map) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  const char* why = comet::plan_channel_perm(absmax, K, G, outlier_ratio, max_frac_8bit, perm,
+                                             group_prec_map, n_outliers);
+  if (why) return fail(COMET_ERR_INVALID_ARG, "%s", why);
+  return ok();
+}
+
+comet_status_t comet_kv4_quantize(const uint16_t* X, uint8_t* codes, uint16_t* params, int T,
+                                  int C, int G, hipStream_t stream) {
+  if (!X || !codes || !params) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (G != 32 && G != 64 && G != 128)
+    return fail(COMET_ERR_UNSUPPORTED, "G=%d: KV4 groups of 32, 64 or 128 channels", G);
+  if (T < 1 || C < G || C % G)
+    return fail(COMET_ERR_INVALID_ARG, "T=%d must be >= 1 and C=%d a positive multiple of G", T,
+                C);
+  if (!aligned16(X) || (reinterpret_cast<uintptr_t>(codes) & 3u) ||
+      (reinterpret_cast<uintptr_t>(params) & 3u))
+    return fail(COMET_ERR_INVALID_ARG, "X must be 16-byte, codes and params 4-byte aligned");
+  comet_status_t st;
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  return launched(comet::launch_kv4_quantize(X, codes, params, T, C, G, stream),
+                  "kv4_quantize launch");
+}
+
+comet_status_t comet_kv4_dequantize(const uint8_t* codes, const uint16_t* params, uint16_t* out,
+                                    int T, int C, int G, hipStream_t stream) {
+  if (!codes || !params || !out) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (G != 32 && G != 64 && G != 128)
+    return fail(COMET_ERR_UNSUPPORTED, "G=%d: KV4 groups of 32, 64 or 128 channels", G);
+  if (T < 1 || C < G || C % G)
+    return fail(COMET_ERR_INVALID_ARG, "T=%d must be >= 1 and C=%d a positive multiple of G", T,
+                C);
+  if (!aligned16(out) || (reinterpret_cast<uintptr_t>(codes) & 3u) ||
+      (reinterpret_cast<uintptr_t>(params) & 3u))
+    return fail(COMET_ERR_INVALID_ARG, "out must be 16-byte, codes and params 4-byte aligned");
+  comet_status_t st;
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  return launched(comet::launch_kv4_dequantize(codes, params, out, T, C, G, stream),
+                  "kv4_dequantize launch");
 }
 
 comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* prec,

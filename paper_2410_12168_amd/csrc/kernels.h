@@ -48,10 +48,22 @@ struct GemmArgs {
   BlockMap map;
 };
 
-hipError_t launch_quantize_act(const uint16_t* X, uint8_t* A, uint16_t* sa, int M, int K,
-                               const BlockMap& map, hipStream_t stream);
-hipError_t launch_pack_w4(const uint16_t* W, uint8_t* Wp, uint16_t* sw, int N, int K,
-                          hipStream_t stream);
+// perm == nullptr: no channel permutation.
+hipError_t launch_quantize_act(const uint16_t* X, const int32_t* perm, uint8_t* A, uint16_t* sa,
+                               int M, int K, const BlockMap& map, hipStream_t stream);
+hipError_t launch_pack_w4(const uint16_t* W, const int32_t* perm, uint8_t* Wp, uint16_t* sw,
+                          int N, int K, hipStream_t stream);
+hipError_t launch_channel_absmax(const uint16_t* X, float* absmax, int M, int K,
+                                 hipStream_t stream);
+// Host: calibration map and channel permutation from per-channel maxima.
+// Returns nullptr on success, else a message.
+const char* plan_channel_perm(const float* absmax, int K, int G, float ratio, float max_frac8,
+                              int32_t* perm, uint8_t* prec, int* n_outliers);
+// KV4 group quantizer; G in {32, 64, 128}.
+hipError_t launch_kv4_quantize(const uint16_t* X, uint8_t* codes, uint16_t* params, int T, int C,
+                               int G, hipStream_t stream);
+hipError_t launch_kv4_dequantize(const uint8_t* codes, const uint16_t* params, uint16_t* out,
+                                 int T, int C, int G, hipStream_t stream);
 
 // Output tile of one GEMM workgroup.
 constexpr int kTileM = 256;

@@ -9,9 +9,17 @@
 // row.  Each lane then emits one packed dword (4-bit) or two (8-bit), so a
 // wave writes 256 B (4-bit) or 512 B (8-bit) of contiguous packed output.
 // The kernels are HBM-bound: 2 bytes in per channel, 0.5 or 1 byte out.
+//
+// Channel permutation (Sec. 3.2): with a permutation the lane gathers its 8
+// channels X[m][perm[c]] instead of loading them as one vector; the indices
+// are the same for every row, so they stay in the caches.  An index outside
+// [0, K) (compared unsigned, so negative ones too) reads channel K-1: no read
+// leaves the row.
 #include <hip/hip_runtime.h>
 #include <hip/hip_fp16.h>
 #include <stdint.h>
+
+#include <algorithm>
 
 #include "kernels.h"
 
@@ -79,6 +87,16 @@ __device__ inline void load8(const uint16_t* p, float (&x)[8]) {
   }
 }
 
+// The 8 channels perm[c0 .. c0+8) of one row, gathered one by one.
+__device__ inline void gather8(const uint16_t* row, const int32_t* perm, int K, float (&x)[8]) {
+  uint4 i0 = *reinterpret_cast<const uint4*>(perm);
+  uint4 i1 = *reinterpret_cast<const uint4*>(perm + 4);
+  uint32_t idx[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+  const uint32_t last = (uint32_t)(K - 1);
+  #pragma unroll
+  for (int i = 0; i < 8; ++i) x[i] = __half2float(__ushort_as_half(row[min(idx[i], last)]));
+}
+
 __device__ inline float max16(float v) {
   // butterfly over the 16 lanes of one (row, block) pair
   v = fmaxf(v, __shfl_xor(v, 1, 16));
@@ -98,7 +116,9 @@ __device__ inline int n8_before(const BlockMap& map, int g) {
 // Activations: pair p -> (block g = p / M, row m = p % M), so the pairs of one
 // workgroup are consecutive rows of one block and their packed outputs are
 // contiguous in the block-major A_packed.
+template <bool kPerm>
 __global__ __launch_bounds__(256) void quantize_act_kernel(const uint16_t* __restrict__ X,
+                                                           const int32_t* __restrict__ perm,
                                                            uint8_t* __restrict__ A,
                                                            uint16_t* __restrict__ sa, int M,
                                                            int K, long long npairs, BlockMap map) {
@@ -110,7 +130,10 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(const uint16_t* __res
   const int m = (int)(pc % M);
   const bool b8 = (map.bits[g >> 6] >> (g & 63)) & 1;
   float x[8];
-  load8(X + (size_t)m * K + (size_t)g * kG + 8 * lane16, x);
+  if (kPerm)
+    gather8(X + (size_t)m * K, perm + (size_t)g * kG + 8 * lane16, K, x);
+  else
+    load8(X + (size_t)m * K + (size_t)g * kG + 8 * lane16, x);
   float a = 0.0f;
   #pragma unroll
   for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
@@ -129,7 +152,9 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(const uint16_t* __res
 
 // Weights: pair p -> (row n = p / NG, block g = p % NG); consecutive pairs are
 // consecutive blocks of one row, contiguous in the row-major W_packed.
+template <bool kPerm>
 __global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t* __restrict__ W,
+                                                      const int32_t* __restrict__ perm,
                                                       uint8_t* __restrict__ Wp,
                                                       uint16_t* __restrict__ sw, int N, int K,
                                                       long long npairs) {
@@ -141,7 +166,10 @@ __global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t* __restrict
   const int n = (int)(pc / NG);
   const int g = (int)(pc % NG);
   float x[8];
-  load8(W + (size_t)n * K + (size_t)g * kG + 8 * lane16, x);
+  if (kPerm)
+    gather8(W + (size_t)n * K, perm + (size_t)g * kG + 8 * lane16, K, x);
+  else
+    load8(W + (size_t)n * K + (size_t)g * kG + 8 * lane16, x);
   float a = 0.0f;
   #pragma unroll
   for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
@@ -153,23 +181,84 @@ __global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t* __restrict
   if (lane16 == 0) sw[(size_t)g * N + n] = s16;
 }
 
+// Per-channel running maximum of |X| over rows (the sampling step of the
+// calibration, Sec. 3.2).  A lane owns 8 channels (one 16-byte load per row),
+// a wave 512 channels; the 4 waves of a workgroup take every 4th row of the
+// workgroup's row range, combine through LDS, and one lane per channel merges
+// into absmax with an unsigned atomic max (non-negative fp32 values order like
+// their bit patterns).  Bit-exact for any split: max is order-free.
+__global__ __launch_bounds__(256) void channel_absmax_kernel(const uint16_t* __restrict__ X,
+                                                             float* __restrict__ absmax, int M,
+                                                             int K, int rows_per_wg) {
+  __shared__ float red[4][64][9];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int c0 = (blockIdx.x * 64 + lane) * 8;
+  const int r0 = blockIdx.y * rows_per_wg;
+  const int r1 = min(M, r0 + rows_per_wg);
+  float a[8];
+  #pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = 0.0f;
+  if (c0 < K) {
+    for (int r = r0 + wave; r < r1; r += 4) {
+      float x[8];
+      load8(X + (size_t)r * K + c0, x);
+      #pragma unroll
+      for (int i = 0; i < 8; ++i) a[i] = fmaxf(a[i], fabsf(x[i]));
+    }
+  }
+  #pragma unroll
+  for (int i = 0; i < 8; ++i) red[wave][lane][i] = a[i];
+  __syncthreads();
+  // thread t merges channel c0(t / 8 lane) + t % 8 over the four waves
+  const int l = threadIdx.x >> 3, i = threadIdx.x & 7;
+  for (int h = 0; h < 2; ++h) {
+    const int ll = l + 32 * h;
+    const int c = (blockIdx.x * 64 + ll) * 8 + i;
+    if (c < K) {
+      float v = fmaxf(fmaxf(red[0][ll][i], red[1][ll][i]), fmaxf(red[2][ll][i], red[3][ll][i]));
+      atomicMax(reinterpret_cast<unsigned int*>(absmax + c), __float_as_uint(v));
+    }
+  }
+}
+
 }  // namespace
 
-hipError_t launch_quantize_act(const uint16_t* X, uint8_t* A, uint16_t* sa, int M, int K,
-                               const BlockMap& map, hipStream_t stream) {
+hipError_t launch_quantize_act(const uint16_t* X, const int32_t* perm, uint8_t* A, uint16_t* sa,
+                               int M, int K, const BlockMap& map, hipStream_t stream) {
   long long npairs = (long long)M * (K / kG);
   long long blocks = (npairs + 15) / 16;
-  hipLaunchKernelGGL(quantize_act_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, X, A, sa,
-                     M, K, npairs, map);
+  if (perm)
+    hipLaunchKernelGGL(quantize_act_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       X, perm, A, sa, M, K, npairs, map);
+  else
+    hipLaunchKernelGGL(quantize_act_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       X, perm, A, sa, M, K, npairs, map);
   return hipGetLastError();
 }
 
-hipError_t launch_pack_w4(const uint16_t* W, uint8_t* Wp, uint16_t* sw, int N, int K,
-                          hipStream_t stream) {
+hipError_t launch_pack_w4(const uint16_t* W, const int32_t* perm, uint8_t* Wp, uint16_t* sw,
+                          int N, int K, hipStream_t stream) {
   long long npairs = (long long)N * (K / kG);
   long long blocks = (npairs + 15) / 16;
-  hipLaunchKernelGGL(pack_w4_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, W, Wp, sw, N,
-                     K, npairs);
+  if (perm)
+    hipLaunchKernelGGL(pack_w4_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, W,
+                       perm, Wp, sw, N, K, npairs);
+  else
+    hipLaunchKernelGGL(pack_w4_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, W,
+                       perm, Wp, sw, N, K, npairs);
+  return hipGetLastError();
+}
+
+hipError_t launch_channel_absmax(const uint16_t* X, float* absmax, int M, int K,
+                                 hipStream_t stream) {
+  const int gx = (K + 511) / 512;
+  // enough row slices to fill the chip, at least 16 rows per workgroup
+  int gy = std::max(1, std::min((M + 15) / 16, std::max(1, 2048 / gx)));
+  const int rows = (M + gy - 1) / gy;
+  gy = (M + rows - 1) / rows;
+  hipLaunchKernelGGL(channel_absmax_kernel, dim3(gx, gy), dim3(256), 0, stream, X, absmax, M, K,
+                     rows);
   return hipGetLastError();
 }
 

@@ -1,0 +1,204 @@
+"""GPU parity of the calibration step, the channel permutation and the KV4
+quantizer (Sec. 3.2; Sec. 6 setup) against the CPU oracle, through the C ABI.
+
+All of it is integer, byte or exactly-defined fp work: maxima, packed codes,
+scales, permutations and KV4 codes/params/reconstructions must be
+bit-identical.  The end-to-end permuted GEMM meets the tolerance of
+tests/parity.py against the oracle on the permuted operands.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2410_12168_amd as comet
+import synth
+from parity import act_rows, assert_out_close
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def dev_u16(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(DEV).view(torch.float16)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def host_u16(t):
+    return host(t.view(torch.int16)).view(np.uint16)
+
+
+def dev_i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(DEV)
+
+
+# --- per-channel maxima ---------------------------------------------------------
+
+@pytest.mark.parametrize("M,K", [(1, 8), (37, 384), (1000, 1032), (33, 4104), (4096, 8192)])
+def test_channel_absmax_bit_exact(M, K):
+    print(f"channel_absmax M={M} K={K}", flush=True)
+    ch = synth.outlier_channels(K, max(1, K // 200), seed=M)
+    X16 = synth.calibration_activations(M, M, K, ch)
+    got = host(comet.channel_absmax(dev_u16(X16)))
+    assert np.array_equal(got.view(np.uint32), oracle.channel_absmax(X16).view(np.uint32))
+
+
+def test_channel_absmax_accumulates():
+    K = 2048
+    X1 = synth.calibration_activations(1, 300, K, [3, 900])
+    X2 = synth.calibration_activations(2, 77, K, [1500])
+    a = comet.channel_absmax(dev_u16(X1))
+    comet.channel_absmax(dev_u16(X2), a)
+    want = oracle.channel_absmax(X2, oracle.channel_absmax(X1))
+    assert np.array_equal(host(a), want)
+
+
+# --- permuted quantization and packing -----------------------------------------
+
+def random_perm(K, seed):
+    return np.random.default_rng(seed).permutation(K).astype(np.int32)
+
+
+PERM_SHAPES = [(1, 128, "random"), (16, 1024, "planned"), (100, 1152, "random"),
+               (257, 640, "planned"), (3, 256, "identity")]
+
+
+def perm_for(kind, X16, K, seed):
+    if kind == "identity":
+        return np.arange(K, dtype=np.int32), np.full(K // 128, 4, np.uint8)
+    if kind == "random":
+        return random_perm(K, seed), synth.prec_map(K // 128, max(1, K // 384), "random", seed)
+    perm, prec, _ = oracle.plan_channel_perm(oracle.channel_absmax(X16), 128, 8.0, 0.25)
+    return perm, prec
+
+
+@pytest.mark.parametrize("M,K,kind", PERM_SHAPES)
+def test_quantize_act_perm_bit_exact(M, K, kind):
+    print(f"quantize_act_perm M={M} K={K} {kind}", flush=True)
+    ch = synth.outlier_channels(K, 3, seed=K)
+    X16 = synth.calibration_activations(M + 1, M, K, ch)
+    perm, prec = perm_for(kind, X16, K, M)
+    A, sa = comet.quantize_act(dev_u16(X16), prec, perm=dev_i32(perm))
+    qa, sa_ref = oracle.quantize_act(oracle.permute_columns(X16, perm), prec)
+    assert np.array_equal(host_u16(sa), sa_ref)
+    assert np.array_equal(host(A), oracle.pack_act(qa, prec))
+
+
+@pytest.mark.parametrize("N,K,kind", [(16, 128, "random"), (48, 1024, "planned"),
+                                      (400, 640, "random")])
+def test_pack_w4_perm_bit_exact(N, K, kind):
+    print(f"pack_w4_perm N={N} K={K} {kind}", flush=True)
+    W16 = synth.weights(N, N, K)
+    X16 = synth.calibration_activations(5, 32, K, synth.outlier_channels(K, 3, seed=1))
+    perm, _ = perm_for(kind, X16, K, N)
+    Wp, sw = comet.pack_w4(dev_u16(W16), perm=dev_i32(perm))
+    qw, sw_ref = oracle.quantize_weight(oracle.permute_columns(W16, perm))
+    assert np.array_equal(host_u16(sw), sw_ref)
+    assert np.array_equal(host(Wp), oracle.pack_weight(qw))
+
+
+def test_perm_null_equals_unpermuted():
+    M, K = 40, 512
+    X16 = synth.activations(3, M, K, np.array([4, 8, 4, 4], np.uint8))
+    prec = np.array([4, 8, 4, 4], np.uint8)
+    X = dev_u16(X16)
+    A0, s0 = comet.quantize_act(X, prec)
+    A1, s1 = comet.quantize_act(X, prec, perm=dev_i32(np.arange(K)))
+    assert torch.equal(A0, A1) and torch.equal(s0.view(torch.int16), s1.view(torch.int16))
+
+
+def test_perm_out_of_range_reads_last_channel():
+    M, K = 8, 256
+    X16 = synth.normal_fp16(9, 1, (M, K))
+    perm = random_perm(K, 2)
+    perm[[3, 100, 200]] = [K, -1, 1 << 30]
+    prec = np.array([8, 4], np.uint8)
+    A, sa = comet.quantize_act(dev_u16(X16), prec, perm=dev_i32(perm))
+    clamped = np.where((perm < 0) | (perm >= K), K - 1, perm).astype(np.int32)
+    qa, sa_ref = oracle.quantize_act(oracle.permute_columns(X16, clamped), prec)
+    assert np.array_equal(host_u16(sa), sa_ref)
+    assert np.array_equal(host(A), oracle.pack_act(qa, prec))
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 256, 1024), (5, 96, 2048)])
+def test_calibrated_gemm_end_to_end(M, N, K):
+    """Sample -> plan -> permuted quantize/pack -> W4Ax GEMM, against the oracle on
+    the permuted operands; and the permutation's purpose: a smaller error than
+    all-4-bit quantization of the unpermuted activations."""
+    print(f"calibrated gemm M={M} N={N} K={K}", flush=True)
+    ch = synth.outlier_channels(K, 7, seed=K)
+    calib = synth.calibration_activations(11, 256, K, ch)
+    absmax = comet.channel_absmax(dev_u16(calib))
+    perm, prec, nout = comet.plan_channel_perm(absmax, 128, 8.0, 0.2)
+    assert nout >= 7 and (prec == 8).sum() == 1
+    X16 = synth.calibration_activations(12, M, K, ch, tid=synth.TID_X)
+    W16 = synth.weights(13, N, K)
+    pd = dev_i32(perm)
+    A, sa = comet.quantize_act(dev_u16(X16), prec, perm=pd)
+    Wp, sw = comet.pack_w4(dev_u16(W16), perm=pd)
+    out = host_u16(comet.w4ax_gemm(A, prec, sa, Wp, sw, M, N, K)).view(np.float16)
+    qa, sa_r = oracle.quantize_act(oracle.permute_columns(X16, perm), prec)
+    qw, sw_r = oracle.quantize_weight(oracle.permute_columns(W16, perm))
+    ref = oracle.dequant_gemm(qa, sa_r, qw, sw_r)
+    assert_out_close(out, ref)
+    exact = oracle.exact_gemm(X16, W16)
+    all4 = np.full(K // 128, 4, np.uint8)
+    A4, sa4 = comet.quantize_act(dev_u16(X16), all4)
+    Wp4, sw4 = comet.pack_w4(dev_u16(W16))
+    out4 = host_u16(comet.w4ax_gemm(A4, all4, sa4, Wp4, sw4, M, N, K)).view(np.float16)
+    e_perm = np.abs(out.astype(np.float64) - exact).mean()
+    e_all4 = np.abs(out4.astype(np.float64) - exact).mean()
+    assert e_perm < 0.7 * e_all4
+
+
+def test_llama3_70b_permuted_quantize_full_size_sampled_rows():
+    """K = 8192 hidden size, 4096 tokens, a planned permutation; rows sampled."""
+    M, K = 4096, 8192
+    print(f"permuted quantize full size M={M} K={K}", flush=True)
+    ch = synth.outlier_channels(K, 41, seed=70)
+    X16 = synth.calibration_activations(70, M, K, ch)
+    absmax = comet.channel_absmax(dev_u16(X16[:512]))
+    perm, prec, _ = comet.plan_channel_perm(absmax, 128, 8.0, 0.2)
+    A, sa = comet.quantize_act(dev_u16(X16), prec, perm=dev_i32(perm))
+    rows = np.array([0, 1, 777, 2048, 4095])
+    qa, sa_ref = oracle.quantize_act(oracle.permute_columns(X16[rows], perm), prec)
+    assert np.array_equal(host_u16(sa)[:, rows], sa_ref)
+    assert np.array_equal(act_rows(host(A), prec, M, rows), oracle.pack_act(qa, prec))
+
+
+# --- KV4 ---------------------------------------------------------------------------
+
+KV_SHAPES = [(1, 128, 128), (7, 1024, 128), (5, 96, 32), (33, 320, 64), (4096, 1024, 128),
+             (3, 64, 64)]
+
+
+@pytest.mark.parametrize("T,C,G", KV_SHAPES)
+def test_kv4_bit_exact(T, C, G):
+    print(f"kv4 T={T} C={C} G={G}", flush=True)
+    X16 = synth.kv_rows(T, T, C)
+    codes, params = comet.kv4_quantize(dev_u16(X16), G)
+    c_ref, p_ref = oracle.kv4_quantize(X16, G)
+    assert np.array_equal(host(codes), c_ref)
+    assert np.array_equal(host_u16(params), p_ref)
+    xr = comet.kv4_dequantize(codes, params, G)
+    assert np.array_equal(host_u16(xr), oracle.kv4_dequantize(c_ref, p_ref, G))
+
+
+def test_kv4_edge_values():
+    C, G = 256, 128
+    rows = [np.zeros(C), np.full(C, 3.5), np.linspace(-65504, 65504, C),
+            np.where(np.arange(C) % 2 == 0, 65504.0, -65504.0), np.full(C, -0.0),
+            np.linspace(0, 6e-8, C),
+            np.where(np.arange(C) % 3 == 0, 0.0, np.where(np.arange(C) % 3 == 1, -0.0, 1.0)),
+            np.where(np.arange(C) % 3 == 0, -0.0, np.where(np.arange(C) % 3 == 1, 0.0, -0.0))]
+    X16 = np.stack([np.asarray(r, np.float32).astype(np.float16).view(np.uint16) for r in rows])
+    codes, params = comet.kv4_quantize(dev_u16(X16), G)
+    c_ref, p_ref = oracle.kv4_quantize(X16, G)
+    assert np.array_equal(host(codes), c_ref)
+    assert np.array_equal(host_u16(params), p_ref)
+    assert np.array_equal(host_u16(comet.kv4_dequantize(codes, params, G)),
+                          oracle.kv4_dequantize(c_ref, p_ref, G))

@@ -135,6 +135,16 @@ def test_kv4_invariants():
     assert np.all(err <= 0.5 * s[..., None] * (1 + 2.0 ** -9) + ulp16)
 
 
+def test_kv4_zero_minimum_is_positive_zero():
+    # min over {+0, -0, 1}: stored as +0 whichever zero comes first
+    for row in ([0x8000, 0x0000, 0x3C00, 0x3C00], [0x0000, 0x8000, 0x3C00, 0x3C00],
+                [0x8000, 0x8000, 0x8000, 0x8000]):
+        _, params = oracle.kv4_quantize(np.array([row], np.uint16), 4)
+        assert int(params[0, 0, 1]) == 0x0000
+    _, params = oracle.kv4_quantize(np.array([[0x8000, 0x0000, 0x8000, 0x0000]], np.uint16), 4)
+    assert params[0, 0].tolist() == [0, 0]
+
+
 def test_kv4_rejects_bad_arguments():
     X = synth.kv_rows(0, 2, 64)
     with pytest.raises(ValueError):
