@@ -42,6 +42,10 @@ WORKLOADS = {
     "llama3-8b-prefill": dict(M=2048, layers="LLAMA3_8B"),
     # few-token regime: the gate_up layer streams its 4-bit weights from HBM
     "llama3-70b-decode": dict(M=8, layers="LLAMA3_70B", only="gate_up", rotate=6),
+    # KV4 cache quantization of a prefill batch (8 prompts x 4096 tokens): the
+    # K and V rows of every layer (8 KV heads x head_dim 128 = 1024 channels,
+    # groups of 128)
+    "llama3-70b-kv4": dict(T=32768, C=1024, n_layers=80, G=128),
 }
 
 # Sources that determine each GEMM kernel's code; a counter summary applies
@@ -96,6 +100,10 @@ def parse():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one device-to-device copy of this many MiB (a "
                          "known-size reference for HBM byte counters)")
+    ap.add_argument("--perm", action="store_true",
+                    help="calibrated channel permutation: activations with scattered outlier "
+                         "channels, map and permutation planned from sampled maxima, permuted "
+                         "quantization (weights packed with the same permutation)")
     ap.add_argument("--cpu-rows", type=int, default=512,
                     help="token rows per layer in the CPU-oracle sample (0: skip)")
     return ap.parse_args()
@@ -116,6 +124,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     wl = WORKLOADS[args.workload]
+    if "T" in wl:
+        return bench_kv4(args, wl, dev)
     M = args.m or wl["M"]
     shapes = getattr(synth, wl["layers"])
     if "only" in wl:
@@ -128,13 +138,24 @@ def main():
         if name not in wanted:
             continue
         NG = K // 128
-        n8 = int(round(NG * args.frac8))
-        prec = synth.prec_map(NG, n8)
-        X16 = synth.activations(args.seed, M, K, prec)
+        perm = None
         W16 = synth.weights(args.seed, N, K)
-        X = torch.from_numpy(X16.view(np.int16)).to(dev).view(torch.float16)
         Wd = torch.from_numpy(W16.view(np.int16)).to(dev).view(torch.float16)
-        Wp, sw = comet.pack_w4(Wd)
+        if args.perm:
+            # outliers on 0.5% of the channels, scattered; calibrate on 512 rows
+            ch = synth.outlier_channels(K, max(1, K // 200), seed=args.seed)
+            X16 = synth.calibration_activations(args.seed, M, K, ch)
+            X = torch.from_numpy(X16.view(np.int16)).to(dev).view(torch.float16)
+            absmax = comet.channel_absmax(X[:512])
+            perm_h, prec, _ = comet.plan_channel_perm(absmax, 128, 8.0, 0.2)
+            perm = torch.from_numpy(perm_h).to(dev)
+            n8 = int((prec == 8).sum())
+        else:
+            n8 = int(round(NG * args.frac8))
+            prec = synth.prec_map(NG, n8)
+            X16 = synth.activations(args.seed, M, K, prec)
+            X = torch.from_numpy(X16.view(np.int16)).to(dev).view(torch.float16)
+        Wp, sw = comet.pack_w4(Wd, perm=perm)
         torch.cuda.synchronize()
         del Wd
         # several weight copies, used in turn, so that each call streams its
@@ -146,7 +167,8 @@ def main():
         sa = torch.empty((NG, M), dtype=torch.float16, device=dev)
         out = torch.empty((M, N), dtype=torch.float16, device=dev)
         layers.append(dict(name=name, M=M, N=N, K=K, prec=prec, X=X, X16=X16, W16=W16, Wp=Wp,
-                           sw=sw, Wps=Wps, sws=sws, A=A, sa=sa, out=out, n8=n8))
+                           sw=sw, Wps=Wps, sws=sws, A=A, sa=sa, out=out, n8=n8, perm=perm,
+                           perm_h=None if perm is None else perm.cpu().numpy()))
     t_setup = time.time() - t_setup
 
     calls = [0]
@@ -157,7 +179,8 @@ def main():
             j = calls[0] % rotate
             if ev is not None:
                 ev[i][0].record()
-            comet.comet_fmpq_quantize_act(L["X"], L["prec"], L["A"], L["sa"], L["M"], L["K"])
+            comet.comet_fmpq_quantize_act_perm(L["X"], L["perm"], L["prec"], L["A"], L["sa"],
+                                               L["M"], L["K"])
             if ev is not None:
                 ev[i][1].record()
             comet.comet_w4ax_gemm(L["A"], L["prec"], L["sa"], L["Wps"][j], L["sws"][j], L["out"],
@@ -253,9 +276,15 @@ def main():
         "dtype": "fp8",
         "data": "synthetic",
         "config": {
-            "workload": f"{args.workload}: quantize+W4Ax GEMM of {'/'.join(per_layer)} at M={M} "
-                        f"tokens, G=128, {args.frac8:.4g} of activation blocks 8-bit",
-            "M": M, "G": 128, "frac8": args.frac8, "seed": args.seed,
+            "workload": (f"{args.workload}: quantize+W4Ax GEMM of {'/'.join(per_layer)} at M={M} "
+                         f"tokens, G=128, " +
+                         (f"calibrated channel permutation ({', '.join(str(L['n8']) for L in layers)}"
+                          f" 8-bit blocks)" if args.perm else
+                          f"{args.frac8:.4g} of activation blocks 8-bit")),
+            "M": M, "G": 128, "frac8": (round(float(np.mean([L['n8'] / (L['K'] // 128)
+                                                          for L in layers])), 4)
+                                        if args.perm else args.frac8),
+            "perm": bool(args.perm), "seed": args.seed,
             "operands": "int4 weights, int4/int8 activation codes on FP8-E4M3 MFMA, fp32 dequant",
         },
         "roofline": roof,
@@ -291,9 +320,14 @@ def cpu_baseline(layers, rows_per_layer: int) -> dict:
     worst_norm = 0.0
     for L in layers:
         rows = np.arange(min(rows_per_layer, L["M"]))
-        qw, sw = oracle.quantize_weight(L["W16"], nthreads=threads)  # offline step, not timed
+        W16, X16 = L["W16"], L["X16"][rows]
+        if L["perm_h"] is not None:  # offline: permute the weight columns
+            W16 = oracle.permute_columns(W16, L["perm_h"])
+        qw, sw = oracle.quantize_weight(W16, nthreads=threads)  # offline step, not timed
         t0 = time.perf_counter()
-        qa, sa = oracle.quantize_act(L["X16"][rows], L["prec"], nthreads=threads)
+        if L["perm_h"] is not None:
+            X16 = oracle.permute_columns(X16, L["perm_h"])
+        qa, sa = oracle.quantize_act(X16, L["prec"], nthreads=threads)
         ref = oracle.dequant_gemm(qa, sa, qw, sw, nthreads=threads)
         t_total += time.perf_counter() - t0
         ops += 2.0 * len(rows) * L["N"] * L["K"]
@@ -308,6 +342,90 @@ def cpu_baseline(layers, rows_per_layer: int) -> dict:
                             for L in layers) + " (quantize + fp64-dequant GEMM)",
         "parity_max_rel": worst, "parity_norm_rel": worst_norm, "parity_ok": worst <= 2e-3,
     }
+
+
+def bench_kv4(args, wl, dev):
+    """KV4 quantization of a prefill batch's K and V rows, every layer: a step is
+    2 * n_layers launches over distinct buffers (the whole set exceeds the
+    last-level cache, so each launch streams from HBM)."""
+    import torch
+
+    import paper_2410_12168_amd as comet
+    import synth
+
+    T, C, G, nl = (args.m or wl["T"]), wl["C"], wl["G"], wl["n_layers"]
+    t_setup = time.time()
+    X16 = [synth.kv_rows(args.seed + i, T, C) for i in range(2)]
+    base = [torch.from_numpy(x.view(np.int16)).to(dev).view(torch.float16) for x in X16]
+    # distinct copies per (layer, K/V)
+    srcs = [base[i % 2] if i < 2 else base[i % 2].clone() for i in range(2 * nl)]
+    codes = [torch.empty((T, C // 2), dtype=torch.uint8, device=dev) for _ in range(2 * nl)]
+    params = [torch.empty((T, C // G, 2), dtype=torch.float16, device=dev) for _ in range(2 * nl)]
+    torch.cuda.synchronize()
+    t_setup = time.time() - t_setup
+
+    def step(ev=None):
+        for i in range(2 * nl):
+            if ev is not None:
+                ev[i][0].record()
+            comet.comet_kv4_quantize(srcs[i], codes[i], params[i], T, C, G)
+            if ev is not None:
+                ev[i][1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    # per-launch durations: events around each launch, on the launch stream
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(2 * nl)]
+           for _ in range(args.steps)]
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    launch_ms = float(np.mean([e[0].elapsed_time(e[1]) for ek in evs for e in ek]))
+    # algorithmic bytes per launch: fp16 rows in, 4-bit codes and {s, mn} out
+    bpl = T * C * 2 + T * C // 2 + T * (C // G) * 4
+    gbs = bpl / (launch_ms * 1e-3) / 1e9
+    step_gbs = 2 * nl * bpl / (ms_per_step * 1e-3) / 1e9
+    record = {
+        "metric": "KV4 cache quantization effective GB/s (HBM), LLaMA-3-70B K/V rows",
+        "value": round(step_gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp16->int4", "data": "synthetic",
+        "config": {"workload": f"{args.workload}: asymmetric INT4 groups of {G} over K and V rows "
+                               f"of {nl} layers, T={T} tokens x C={C} channels",
+                   "T": T, "C": C, "G": G, "layers": nl, "seed": args.seed},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": f"kv4_quantize, T={T}, C={C}, G={G}: {bpl} bytes per launch, "
+                               f"{launch_ms * 1e3:.2f} us per launch",
+                     "alg_bytes_per_launch": bpl},
+        "setup_s": round(t_setup, 1),
+    }
+    if args.cpu_rows > 0:
+        import oracle
+
+        rows = min(4096, T)
+        threads = 1
+        t0 = time.perf_counter()
+        c_ref, p_ref = oracle.kv4_quantize(X16[0][:rows], G)
+        dt = time.perf_counter() - t0
+        got_c = codes[0][:rows].cpu().numpy()
+        got_p = params[0][:rows].view(torch.int16).cpu().numpy().view(np.uint16)
+        record["cpu_baseline"] = {
+            "value": round((rows * C * 2 + rows * C // 2 + rows * (C // G) * 4) / dt / 1e9, 4),
+            "unit": "GB/s", "cores": threads, "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"first {rows} of {T} K rows of one layer",
+            "parity_ok": bool(np.array_equal(got_c, c_ref) and np.array_equal(got_p, p_ref)),
+        }
+    print(json.dumps(record), flush=True)
 
 
 if __name__ == "__main__":
