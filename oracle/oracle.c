@@ -345,18 +345,27 @@ int orc_plan_channel_perm(const float* absmax, int K, int G, float outlier_ratio
   int cap = (int)floor((double)max_frac8 * (double)NG);
   int n8 = need < cap ? need : cap;
 
-  /* The n8*G highest-ranked channels fill the 8-bit blocks in rank order; the
-   * rest follow in their original order. */
+  /* The n8*G highest-ranked channels fill the 8-bit blocks in rank order.
+   * Every other position keeps its own channel, except the positions those
+   * channels left: they take the channels displaced from the 8-bit blocks,
+   * in ascending order on both sides. */
   for (int c = 0; c < K; ++c) rank[c] = c;
   g_rank_key = absmax;
   qsort(rank, (size_t)K, sizeof(int32_t), cmp_rank);
-  int pos = 0;
-  for (int i = 0; i < n8 * G; ++i) {
-    perm[pos++] = rank[i];
+  const int head = n8 * G;
+  for (int i = 0; i < head; ++i) {
+    perm[i] = rank[i];
     taken[rank[i]] = 1;
   }
-  for (int c = 0; c < K; ++c)
-    if (!taken[c]) perm[pos++] = c;
+  int next_displaced = 0;
+  for (int p = head; p < K; ++p) {
+    if (!taken[p]) {
+      perm[p] = p;
+      continue;
+    }
+    while (taken[next_displaced]) ++next_displaced; /* a head channel not in the head set */
+    perm[p] = next_displaced++;
+  }
   for (int g = 0; g < NG; ++g) prec[g] = g < n8 ? 8 : 4;
   if (n_outliers) *n_outliers = nout;
   free(sorted);

@@ -96,9 +96,12 @@ void orc_exact_gemm(const uint16_t* X, const uint16_t* W, int M, int N, int K, d
  *   (compared in fp64; every channel if ratio <= 0).  The number of 8-bit
  *   blocks is n8 = min(ceil(n_out / G), floor(max_frac8 * K/G)).  Channels are
  *   ranked by absmax descending, ties by index; perm[0 .. n8*G) holds the first
- *   n8*G ranked channels in rank order and perm[n8*G .. K) the rest in
- *   ascending order; prec[g] = 8 for g < n8, else 4.  Returns 0, or -1 for bad
- *   arguments (max_frac8 outside [0, 1], a negative or non-finite maximum). */
+ *   n8*G ranked channels in rank order.  For p >= n8*G, perm[p] = p unless
+ *   channel p moved into the 8-bit blocks; those positions take the channels
+ *   displaced from positions [0, n8*G) (the ones not ranked in), ascending
+ *   channel to ascending position.  prec[g] = 8 for g < n8, else 4.  Returns
+ *   0, or -1 for bad arguments (max_frac8 outside [0, 1], a negative or
+ *   non-finite maximum). */
 int orc_permute_columns(const uint16_t* X, const int32_t* perm, int R, int K, uint16_t* out);
 void orc_channel_absmax(const uint16_t* X, int M, int K, float* absmax);
 int orc_plan_channel_perm(const float* absmax, int K, int G, float outlier_ratio,

@@ -10,8 +10,12 @@
 //              ratio <= 0, which turns the rule into "fill the cap";
 //   n8       = min(ceil(n_out / G), floor(max_frac8 * K/G)) 8-bit blocks;
 //   perm     = the n8*G channels ranked first (absmax descending, ties by
-//              channel index) in rank order, then every other channel in
-//              ascending order, so the 4-bit blocks keep the original order.
+//              channel index) in rank order; every later position keeps its
+//              own channel unless that channel moved up, and those positions
+//              take the channels displaced from the first n8*G positions,
+//              ascending to ascending.  Few channels move, so most 8-channel
+//              chunks of a row stay in place and the fused gather of the
+//              quantizer can read them with one vector load.
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
@@ -53,9 +57,11 @@ const char* plan_channel_perm(const float* absmax, int K, int G, float ratio, fl
     perm[i] = order[i];
     in8[order[i]] = 1;
   }
-  int pos = head;
-  for (int c = 0; c < K; ++c)
-    if (!in8[c]) perm[pos++] = c;
+  std::vector<int32_t> displaced;
+  for (int c = 0; c < head; ++c)
+    if (!in8[c]) displaced.push_back(c);
+  size_t d = 0;
+  for (int p = head; p < K; ++p) perm[p] = in8[p] ? displaced[d++] : p;
   for (int g = 0; g < NG; ++g) prec[g] = g < n8 ? 8 : 4;
   if (n_outliers) *n_outliers = nout;
   return nullptr;

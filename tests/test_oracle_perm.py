@@ -6,7 +6,8 @@ permutation, so the product is unchanged) and quantizes only those blocks to
 8 bits.  Pins, none of which re-types the oracle's steps:
   * hand-worked cases in tests/golden/plan_channel_perm.json;
   * invariants any plan under the reading must satisfy (a permutation; the
-    8-bit blocks hold exactly the largest maxima; the rest keep their order;
+    8-bit blocks hold exactly the largest maxima; every other channel stays
+    put unless it moved up, and the displaced channels fill the gaps;
     the 8-bit share stays under the cap; every outlier is covered when the cap
     allows);
   * numpy brute force for the per-channel maxima and the column gather;
@@ -48,11 +49,18 @@ def check_plan(absmax, G, ratio, frac, perm, prec, nout):
     assert prec.tolist() == [8] * n8 + [4] * (NG - n8)
     assert n8 <= int(np.floor(np.float64(frac) * NG))
     head = perm[: n8 * G]
-    tail = perm[n8 * G:]
     # the 8-bit blocks hold the n8*G largest maxima, in descending order
     assert np.array_equal(np.sort(absmax[head]), np.sort(absmax)[K - n8 * G:])
     assert np.all(np.diff(absmax[head].astype(np.float64)) <= 0)
-    assert np.all(np.diff(tail) > 0)
+    # later positions keep their channel unless it moved up; the vacated
+    # positions take the displaced channels, ascending to ascending
+    moved = np.zeros(K, bool)
+    moved[head] = True
+    pos = np.arange(n8 * G, K)
+    keep = ~moved[pos]
+    assert np.array_equal(perm[pos[keep]], pos[keep])
+    displaced = np.array([c for c in range(n8 * G) if not moved[c]], dtype=np.int64)
+    assert np.array_equal(perm[pos[~keep]], displaced)
     med = np.sort(absmax)[(K - 1) // 2]
     out = np.flatnonzero(absmax.astype(np.float64) > np.float64(ratio) * np.float64(med))
     if ratio > 0:
