@@ -54,6 +54,7 @@ CSRC = os.path.join(ROOT, "paper_2410_12168_amd", "csrc")
 KERNEL_SOURCES = {
     "tile": ["gemm.hip", "operand.h", "kernels.h"],
     "skinny": ["gemm_skinny.hip", "operand.h", "kernels.h"],
+    "kv4": ["kv4.hip"],
 }
 SKINNY_MAX_M = 64  # the library runs the few-token kernel up to this M
 
@@ -66,10 +67,16 @@ def kernel_sha(kind: str) -> str:
     return h.hexdigest()
 
 
+def profile_path(kind: str, workload: str, layer: str, M: int) -> str:
+    if kind == "kv4":
+        return os.path.join(ROOT, "profiles", f"kv4_quantize_{workload}_t{M}.txt")
+    return os.path.join(ROOT, "profiles", f"w4ax_gemm_{kind}_{workload}_{layer}_m{M}.txt")
+
+
 def profiled_traffic(kind: str, workload: str, layer: str, M: int):
     """HBM bytes per launch from the committed counter summary of this kernel
     and workload, or None (no summary, or the kernel changed since)."""
-    path = os.path.join(ROOT, "profiles", f"w4ax_gemm_{kind}_{workload}_{layer}_m{M}.txt")
+    path = profile_path(kind, workload, layer, M)
     if not os.path.exists(path):
         return None
     fields = {}
@@ -403,12 +410,19 @@ def bench_kv4(args, wl, dev):
                                f"of {nl} layers, T={T} tokens x C={C} channels",
                    "T": T, "C": C, "G": G, "layers": nl, "seed": args.seed},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": profiled_traffic("kv4", args.workload, "kv", T),
                      "kernel": f"kv4_quantize, T={T}, C={C}, G={G}: {bpl} bytes per launch, "
                                f"{launch_ms * 1e3:.2f} us per launch",
                      "alg_bytes_per_launch": bpl},
         "setup_s": round(t_setup, 1),
     }
+    if args.copy_mib > 0:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        record["copy_mib"] = args.copy_mib
     if args.cpu_rows > 0:
         import oracle
 

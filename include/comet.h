@@ -88,6 +88,7 @@ COMET_API size_t comet_act_packed_bytes(const uint8_t* group_prec_map, int M, in
  *   X        device, fp16 [M][K] row-major, 16-byte aligned.
  *   A_packed device, comet_act_packed_bytes(...) bytes, 16-byte aligned.
  *   a_scales device, fp16 [K/G][M].
+ * M may be at most 2,097,120 (COMET_ERR_UNSUPPORTED beyond).
  * Non-finite inputs are not supported (the codes they produce are unspecified). */
 COMET_API comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* group_prec_map,
                                        uint8_t* A_packed, uint16_t* a_scales, int M, int K,
@@ -139,8 +140,11 @@ COMET_API comet_status_t comet_channel_absmax(const uint16_t* X, float* absmax, 
  *   outlier channels: absmax > outlier_ratio * med, compared in fp64
  *                     (every channel when outlier_ratio <= 0);
  *   n8 = min(ceil(n_out / G), floor(max_frac_8bit * K/G)) 8-bit blocks;
- *   perm (host int32 [K]): the n8*G channels with the largest maxima (ties by
- *        index) in that order, then every other channel in ascending order;
+ *   perm (host int32 [K]): positions [0, n8*G) hold the n8*G channels with
+ *        the largest maxima (ties by index) in that order; a later position p
+ *        holds channel p unless channel p moved up, and those positions hold
+ *        the channels displaced from [0, n8*G), ascending to ascending (few
+ *        channels move, which keeps the fused gather cheap);
  *   group_prec_map (host uint8 [K/G]): 8 for g < n8, else 4;
  *   *n_outliers (may be NULL): n_out.
  * G is any positive divisor of K here (the GEMM needs 128).  Errors:

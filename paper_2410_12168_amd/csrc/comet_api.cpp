@@ -37,6 +37,9 @@ comet_status_t ok() {
   return COMET_OK;
 }
 
+// The activation quantizer's grid has one row of workgroups per 32 tokens.
+constexpr int kMaxQuantRows = 65535 * 32;
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Checks shared by every entry point: G, K and the block map.
@@ -351,6 +354,8 @@ comet_status_t comet_fmpq_quantize_act_perm(const uint16_t* X, const int32_t* pe
                                             hipStream_t stream) {
   if (!X || !A_packed || !a_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
   if (M < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d must be >= 1", M);
+  if (M > kMaxQuantRows)
+    return fail(COMET_ERR_UNSUPPORTED, "M=%d exceeds %d rows per call", M, kMaxQuantRows);
   comet_status_t st = check_kg(K, G);
   if (st) return st;
   if (!aligned16(X) || !aligned16(A_packed) || !aligned16(a_scales) || !aligned16(perm))

@@ -11,6 +11,10 @@
 // Layout: codes [T][C/2] bytes (channel 2j in the low nibble of byte j),
 // params fp16 [T][C/G][2] = {s, mn}.
 //
+// The division (x - mn) / s uses one correctly rounded reciprocal per lane and
+// Markstein's correction step (two fmas per element), exact for a binary16 s;
+// quantize.hip gives the argument.
+//
 // Work decomposition: a lane owns 8 consecutive channels (one 16-byte load);
 // G/8 lanes share a group and reduce min/max with xor shuffles.  Groups are
 // numbered row-major, so a wave reads 1 KB of contiguous fp16 and writes
@@ -25,6 +29,8 @@
 namespace comet {
 
 namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 template <int L>
 __device__ inline float group_min(float v) {
@@ -49,7 +55,8 @@ __global__ __launch_bounds__(256) void kv4_quantize_kernel(const uint16_t* __res
   const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
   const bool valid = t < nlanes;
   const long long tc = valid ? t : nlanes - 1;
-  uint4 v = *reinterpret_cast<const uint4*>(X + 8 * tc);
+  // read once: nontemporal, so the rows do not displace cached data
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(X + 8 * tc));
   uint32_t w[4] = {v.x, v.y, v.z, v.w};
   float x[8];
   #pragma unroll
@@ -71,18 +78,18 @@ __global__ __launch_bounds__(256) void kv4_quantize_kernel(const uint16_t* __res
   const float range = mx - mn;
   const __half h = __float2half_rn(range / 15.0f);
   const float s = __half2float(h);
+  const float r = s != 0.0f ? 1.0f / s : 0.0f;  // s == 0 gives q = 0
   uint32_t packed = 0;
   #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    float r = 0.0f;
-    if (s != 0.0f) {
-      r = rintf((x[i] - mn) / s);
-      r = fminf(fmaxf(r, 0.0f), 15.0f);
-    }
-    packed |= (uint32_t)r << (4 * i);
+    const float a = x[i] - mn;
+    const float q0 = a * r;
+    const float q = fmaf(fmaf(-q0, s, a), r, q0);  // RN(a / s)
+    packed |= (uint32_t)fminf(rintf(q), 15.0f) << (4 * i);
   }
   if (!valid) return;
-  *reinterpret_cast<uint32_t*>(codes + 4 * tc) = packed;
+  // the cache is read back much later: keep the codes out of the caches too
+  __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(codes + 4 * tc));
   if ((threadIdx.x & (L - 1)) == 0) {
     const uint32_t p = (uint32_t)__half_as_ushort(h) |
                        ((uint32_t)__half_as_ushort(__float2half_rn(mn)) << 16);

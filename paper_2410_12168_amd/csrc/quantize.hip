@@ -8,11 +8,29 @@
 // (one 128-bit load of fp16).  The 16-lane max reduction stays inside a DPP
 // row.  Each lane then emits one packed dword (4-bit) or two (8-bit), so a
 // wave writes 256 B (4-bit) or 512 B (8-bit) of contiguous packed output.
-// The kernels are HBM-bound: 2 bytes in per channel, 0.5 or 1 byte out.
+// The activation grid is 2-D (block, row group): no 64-bit index division.
+// 2 bytes in per channel, 0.5 or 1 byte out.
 //
-// Channel permutation (Sec. 3.2): with a permutation the lane gathers its 8
-// channels X[m][perm[c]] instead of loading them as one vector; the indices
-// are the same for every row, so they stay in the caches.  An index outside
+// Division.  The codes need RN(x / s) exactly (IEEE fp32 division), which as
+// a library division costs about ten vector instructions per element and made
+// these kernels ALU-bound.  Instead each lane takes one correctly rounded
+// reciprocal r = RN(1/s) and per element
+//     q0 = RN(x r),  rem = x - q0 s  (one fma, exact),  q = RN(q0 + rem r),
+// Markstein's correction step.  Why q = RN(x / s) here: s is a binary16
+// value, so its significand has at most 11 bits.  q0 is within 2 ulps of x/s,
+// so rem is a multiple of ulp(q0) * 2^e(s) of at most 13 bits: exact.  The
+// fma then sees x/s perturbed by at most |rem| |r - 1/s| <= 2^-46 ulp-units
+// of the result, while x/s, when it is not a midpoint between binary32
+// neighbours, lies at least 2^-35 units from one (x has 24 bits, s 11 bits),
+// and it is never exactly a midpoint (a midpoint needs 25 significant bits
+// times s's odd part).  So rounding the perturbed value gives RN(x / s).  The
+// identity is also checked exhaustively over every binary16 operand pair on
+// the CPU.  s == 0 takes r = 0, which yields q = 0 as the quantizer requires.
+//
+// Channel permutation (Sec. 3.2): with a permutation the lane reads its 8
+// channels X[m][perm[c]]: one vector load where the permutation leaves the
+// chunk in place, one load per channel elsewhere.  The indices are the same
+// for every row: a lane reads them once for all its rows.  An index outside
 // [0, K) (compared unsigned, so negative ones too) reads channel K-1: no read
 // leaves the row.
 #include <hip/hip_runtime.h>
@@ -36,20 +54,26 @@ struct Codes {
 // Scale and codes follow the block quantizer exactly: one IEEE fp32 division
 // for the scale, rounding to binary16 (nearest even), then one IEEE fp32
 // division per element, rint (nearest even) and clamp.
-__device__ inline uint16_t quantize8(const float (&x)[8], float amax, int qmax, Codes& c) {
-  float s32 = amax / (float)qmax;
+// RN(a / s) from r = RN(1/s) for a binary16 s (see the header).
+__device__ inline float div_rn(float a, float s, float r) {
+  const float q0 = a * r;
+  const float rem = fmaf(-q0, s, a);
+  return fmaf(rem, r, q0);
+}
+
+// Magnitudes and signs follow q = clamp(rint(x / s), -qmax, qmax) with the
+// sign taken from x (rint and the division are symmetric); a zero code has a
+// clear sign bit.
+__device__ inline uint16_t quantize8(const float (&x)[8], float amax, float qmax, Codes& c) {
+  float s32 = amax / qmax;
   __half h = __float2half_rn(s32);
   float s = __half2float(h);
+  const float r = s != 0.0f ? 1.0f / s : 0.0f;
   #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    float r = 0.0f;
-    if (s != 0.0f) {
-      r = rintf(x[i] / s);
-      r = fminf(fmaxf(r, (float)-qmax), (float)qmax);
-    }
-    int q = (int)r;
-    c.sign[i] = q < 0 ? 1u : 0u;
-    c.mag[i] = (uint32_t)(q < 0 ? -q : q);
+    const float m = fminf(rintf(div_rn(fabsf(x[i]), s, r)), qmax);
+    c.mag[i] = (uint32_t)m;
+    c.sign[i] = (__float_as_uint(x[i]) >> 31) & (m != 0.0f ? 1u : 0u);
   }
   return __half_as_ushort(h);
 }
@@ -87,11 +111,36 @@ __device__ inline void load8(const uint16_t* p, float (&x)[8]) {
   }
 }
 
-// The 8 channels perm[c0 .. c0+8) of one row, gathered one by one.
-__device__ inline void gather8(const uint16_t* row, const int32_t* perm, int K, float (&x)[8]) {
-  uint4 i0 = *reinterpret_cast<const uint4*>(perm);
-  uint4 i1 = *reinterpret_cast<const uint4*>(perm + 4);
-  uint32_t idx[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16 bytes of fp16 that are read exactly once: nontemporal, so they do not
+// displace cached data.
+__device__ inline void load8_nt(const uint16_t* p, float (&x)[8]) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  #pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __half2float(__ushort_as_half((unsigned short)(w[i] & 0xFFFF)));
+    x[2 * i + 1] = __half2float(__ushort_as_half((unsigned short)(w[i] >> 16)));
+  }
+}
+
+// The permutation indices perm[c0 .. c0+8), and whether they leave the chunk
+// in place (perm[c0 + i] = c0 + i, true of most chunks of a calibrated plan).
+__device__ inline bool perm_chunk(const int32_t* perm, int c0, uint32_t (&idx)[8]) {
+  const uint4 i0 = *reinterpret_cast<const uint4*>(perm + c0);
+  const uint4 i1 = *reinterpret_cast<const uint4*>(perm + c0 + 4);
+  idx[0] = i0.x; idx[1] = i0.y; idx[2] = i0.z; idx[3] = i0.w;
+  idx[4] = i1.x; idx[5] = i1.y; idx[6] = i1.z; idx[7] = i1.w;
+  bool same = true;
+  #pragma unroll
+  for (int i = 0; i < 8; ++i) same = same && idx[i] == (uint32_t)(c0 + i);
+  return same;
+}
+
+// One channel at a time; an index outside [0, K) reads channel K-1.
+__device__ inline void gather8(const uint16_t* row, const uint32_t (&idx)[8], int K,
+                               float (&x)[8]) {
   const uint32_t last = (uint32_t)(K - 1);
   #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = __half2float(__ushort_as_half(row[min(idx[i], last)]));
@@ -113,41 +162,55 @@ __device__ inline int n8_before(const BlockMap& map, int g) {
   return n;
 }
 
-// Activations: pair p -> (block g = p / M, row m = p % M), so the pairs of one
-// workgroup are consecutive rows of one block and their packed outputs are
-// contiguous in the block-major A_packed.
-template <bool kPerm>
+// Activations.  A workgroup owns one block g and 16 * R consecutive rows;
+// 16-lane group q takes rows r0 + q + 16 j, j < R, whose 16-byte loads are all
+// issued before any arithmetic.  Without a permutation (R = 2) the workgroups
+// run block-fastest, so the chip streams whole rows of X at a time, and the
+// loads are nontemporal.  With one (R = 4) they run row-fastest: the rows share
+// the block's permutation indices, read once per lane, and a chunk that the
+// permutation moves is gathered channel by channel.
+template <bool kPerm, int R>
 __global__ __launch_bounds__(256) void quantize_act_kernel(const uint16_t* __restrict__ X,
                                                            const int32_t* __restrict__ perm,
                                                            uint8_t* __restrict__ A,
                                                            uint16_t* __restrict__ sa, int M,
-                                                           int K, long long npairs, BlockMap map) {
+                                                           int K, BlockMap map) {
   const int lane16 = threadIdx.x & 15;
-  const long long p = (long long)blockIdx.x * 16 + (threadIdx.x >> 4);
-  const bool valid = p < npairs;
-  const long long pc = valid ? p : npairs - 1;
-  const int g = (int)(pc / M);
-  const int m = (int)(pc % M);
+  const int g = kPerm ? blockIdx.y : blockIdx.x;
+  const int rows0 = (kPerm ? blockIdx.x : blockIdx.y) * 16 * R + (threadIdx.x >> 4);
+  const int c0 = g * kG + 8 * lane16;
   const bool b8 = (map.bits[g >> 6] >> (g & 63)) & 1;
-  float x[8];
-  if (kPerm)
-    gather8(X + (size_t)m * K, perm + (size_t)g * kG + 8 * lane16, K, x);
-  else
-    load8(X + (size_t)m * K + (size_t)g * kG + 8 * lane16, x);
-  float a = 0.0f;
+  float x[R][8];
   #pragma unroll
-  for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
-  a = max16(a);
-  Codes c;
-  uint16_t s16 = quantize8(x, a, b8 ? 127 : 7, c);
-  if (!valid) return;
-  const size_t base = (size_t)M * 64 * (size_t)(g + n8_before(map, g));
-  if (b8) {
-    *reinterpret_cast<uint2*>(A + base + (size_t)m * 128 + 8 * lane16) = pack8(c);
-  } else {
-    *reinterpret_cast<uint32_t*>(A + base + (size_t)m * 64 + 4 * lane16) = pack4(c);
+  for (int j = 0; j < R; ++j) {
+    const int m = min(rows0 + 16 * j, M - 1);
+    if (kPerm)
+      load8(X + (size_t)m * K + c0, x[j]);
+    else
+      load8_nt(X + (size_t)m * K + c0, x[j]);
   }
-  if (lane16 == 0) sa[(size_t)g * M + m] = s16;
+  bool same = true;
+  uint32_t idx[8];
+  if (kPerm) same = perm_chunk(perm, c0, idx);
+  const size_t base = (size_t)M * 64 * (size_t)(g + n8_before(map, g));
+  #pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int m = rows0 + 16 * j;
+    if (kPerm && !same) gather8(X + (size_t)min(m, M - 1) * K, idx, K, x[j]);
+    float a = 0.0f;
+    #pragma unroll
+    for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[j][i]));
+    a = max16(a);
+    Codes c;
+    const uint16_t s16 = quantize8(x[j], a, b8 ? 127.0f : 7.0f, c);
+    if (m >= M) continue;
+    if (b8) {
+      *reinterpret_cast<uint2*>(A + base + (size_t)m * 128 + 8 * lane16) = pack8(c);
+    } else {
+      *reinterpret_cast<uint32_t*>(A + base + (size_t)m * 64 + 4 * lane16) = pack4(c);
+    }
+    if (lane16 == 0) sa[(size_t)g * M + m] = s16;
+  }
 }
 
 // Weights: pair p -> (row n = p / NG, block g = p % NG); consecutive pairs are
@@ -166,16 +229,18 @@ __global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t* __restrict
   const int n = (int)(pc / NG);
   const int g = (int)(pc % NG);
   float x[8];
-  if (kPerm)
-    gather8(W + (size_t)n * K, perm + (size_t)g * kG + 8 * lane16, K, x);
-  else
-    load8(W + (size_t)n * K + (size_t)g * kG + 8 * lane16, x);
+  const int c0 = g * kG + 8 * lane16;
+  load8(W + (size_t)n * K + c0, x);
+  if (kPerm) {
+    uint32_t idx[8];
+    if (!perm_chunk(perm, c0, idx)) gather8(W + (size_t)n * K, idx, K, x);
+  }
   float a = 0.0f;
   #pragma unroll
   for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
   a = max16(a);
   Codes c;
-  uint16_t s16 = quantize8(x, a, 7, c);
+  uint16_t s16 = quantize8(x, a, 7.0f, c);
   if (!valid) return;
   *reinterpret_cast<uint32_t*>(Wp + (size_t)n * (K / 2) + (size_t)g * 64 + 4 * lane16) = pack4(c);
   if (lane16 == 0) sw[(size_t)g * N + n] = s16;
@@ -226,14 +291,13 @@ __global__ __launch_bounds__(256) void channel_absmax_kernel(const uint16_t* __r
 
 hipError_t launch_quantize_act(const uint16_t* X, const int32_t* perm, uint8_t* A, uint16_t* sa,
                                int M, int K, const BlockMap& map, hipStream_t stream) {
-  long long npairs = (long long)M * (K / kG);
-  long long blocks = (npairs + 15) / 16;
+  const unsigned NG = (unsigned)(K / kG);
   if (perm)
-    hipLaunchKernelGGL(quantize_act_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       X, perm, A, sa, M, K, npairs, map);
+    hipLaunchKernelGGL((quantize_act_kernel<true, 4>), dim3((unsigned)((M + 63) / 64), NG),
+                       dim3(256), 0, stream, X, perm, A, sa, M, K, map);
   else
-    hipLaunchKernelGGL(quantize_act_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       X, perm, A, sa, M, K, npairs, map);
+    hipLaunchKernelGGL((quantize_act_kernel<false, 2>), dim3(NG, (unsigned)((M + 31) / 32)),
+                       dim3(256), 0, stream, X, perm, A, sa, M, K, map);
   return hipGetLastError();
 }
 

@@ -101,4 +101,7 @@ def test_device_entry_points_check_arguments():
     assert L.comet_kv4_quantize(p(FAKE), p(FAKE + 2), p(FAKE), 4, 128, 128, None) == 1
     assert L.comet_kv4_dequantize(p(FAKE), p(FAKE), p(FAKE), 4, 256, 256, None) == 2
     assert L.comet_kv4_dequantize(p(FAKE), p(FAKE), None, 4, 256, 128, None) == 1
+    # the activation quantizer's row limit
+    assert L.comet_fmpq_quantize_act_perm(p(FAKE), None, mp, p(FAKE), p(FAKE), 65535 * 32 + 1, 256,
+                                          128, None) == 2
     assert comet.comet_last_error() != ""
