@@ -154,10 +154,10 @@ std::string sched_mode() {
   return (m && *m) ? std::string(m) : std::string("cost");
 }
 
-comet::PlanOptions plan_options(int cus, const std::string& mode) {
+comet::PlanOptions plan_options(int M, int cus, const std::string& mode) {
   comet::PlanOptions opt;
   opt.num_cus = cus;
-  opt.tile_m = comet::kTileM;
+  opt.tile_m = comet::gemm_tile_m(M);
   opt.tile_n = comet::kTileN;
   opt.mode = mode;
   return opt;
@@ -176,7 +176,7 @@ comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* pr
   }
   DevicePlan dp;
   std::string err;
-  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(cus, mode), &dp.host, &err))
+  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, cus, mode), &dp.host, &err))
     return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
   const comet::Plan& h = dp.host;
   std::vector<int> blob;
@@ -291,7 +291,8 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   Workspace* ws = nullptr;
   if (!skinny && plan->host.partial_slots > 0) {
     const size_t slots = (size_t)plan->host.partial_slots;
-    if ((st = get_workspace(dev, stream, slots * comet::kTileM * comet::kTileN, slots, &ws)))
+    if ((st = get_workspace(dev, stream, slots * plan->host.tile_m * plan->host.tile_n, slots,
+                            &ws)))
       return st;
   }
   a.A = A;
@@ -318,7 +319,8 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   a.win_n1 = n1;
   a.map = map;
   if (skinny) return launched(comet::launch_gemm_skinny(a, diag, stream), "gemm launch");
-  return launched(comet::launch_gemm(a, plan->host.num_wgs, diag, stream), "gemm launch");
+  return launched(comet::launch_gemm(a, plan->host.num_wgs, diag, plan->host.tile_m, stream),
+                  "gemm launch");
 }
 
 }  // namespace
@@ -494,10 +496,7 @@ comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* p
   if (st) return st;
   comet::BlockMap map;
   if ((st = make_map(prec, K / G, &map))) return st;
-  comet::PlanOptions opt;
-  opt.num_cus = num_cus;
-  const char* mode = std::getenv("COMET_SCHED");
-  if (mode && *mode) opt.mode = mode;
+  comet::PlanOptions opt = plan_options(M, num_cus, sched_mode());
   comet::Plan plan;
   std::string err;
   if (!comet::build_plan(M, N, K, G, prec, opt, &plan, &err))

@@ -45,17 +45,26 @@ namespace comet {
 namespace {
 
 constexpr int kThreads = 512;            // 8 waves
-constexpr int kWM = 128, kWN = 64;       // wave quadrant
-constexpr int kRB = kWM / 16, kCB = kWN / 16;
-constexpr int kA = kTileM * 128;          // LDS bytes of one A stage (fp8 or raw 8-bit codes)
-constexpr int kS = 4 * (kTileM + kTileN);  // LDS bytes of one stage's scales (fp32)
-constexpr int kBuf = kA + kS;             // one activation stage, double-buffered
+constexpr int kWN = 64;                  // wave quadrant width
+constexpr int kCB = kWN / 16;
 constexpr int kWr = kTileN * 64;          // one packed weight K-block, ring of three
-constexpr int kLds = 2 * kBuf + 3 * kWr;
+static_assert(kTileN == 4 * kWN, "8 waves as 2 x 4 quadrants");
 
-static_assert(kTileM == 2 * kWM && kTileN == 4 * kWN, "8 waves as 2 x 4 quadrants");
+// Geometry of a tile of TM rows (TM = 256, or 128 for 64 < M <= 128, where a
+// 256-row tile would leave half of every MFMA idle): 8 waves as 2 x 4
+// quadrants of (TM / 2) x 64.
+template <int TM>
+struct Geo {
+  static constexpr int WM = TM / 2;                // wave quadrant rows
+  static constexpr int RB = WM / 16;               // row blocks per wave
+  static constexpr int A = TM * 128;               // LDS bytes of one A stage (fp8 or raw 8-bit codes)
+  static constexpr int S = 4 * (TM + kTileN);      // LDS bytes of one stage's scales (fp32)
+  static constexpr int Buf = A + S;                // one activation stage, double-buffered
+  static constexpr int Lds = 2 * Buf + 3 * kWr;
+  static_assert(TM == 256 || TM == 128, "tile heights");
+};
 
-// LDS layout of one activation stage: A (kTileM rows x 128 B), then the
+// LDS layout of one activation stage: A (TM rows x 128 B), then the
 // tile's fp32 activation scales (times 2^18) and weight scales.  Row r's
 // 16-byte chunk c sits at r*128 + ((c ^ g(r)) << 4) with g(r) = (r ^ (r >> 1))
 // & 7.  With this swizzle the 16 rows of one MFMA operand fetch
@@ -69,15 +78,13 @@ __device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ ((r ^ 
 __device__ __forceinline__ int wswz(int c, int j) { return c * 64 + ((j ^ ((c >> 2) & 3)) << 4); }
 
 // Scales of one stage (floats after the A codes): the activation scale of
-// tile row r = 128 h + 16 rb + 4 j + i at ((h * 8 + rb) * 4 + j) * 4 + i, so a
-// lane's four rows of a row block are one 16-byte read; the weight scale of
-// tile column c = 64 q + 16 cb + x at kTileM + (16 q + x) * 4 + cb, so a
-// lane's column in all four column blocks is one 16-byte read.
-__device__ __forceinline__ int sa_slot(int r) {
-  return (((r >> 7) * 8 + ((r >> 4) & 7)) * 4 + ((r >> 2) & 3)) * 4 + (r & 3);
-}
+// tile row r at r, so a lane's four rows 4 j .. 4 j + 3 of a row block are one
+// 16-byte read; the weight scale of tile column c = 64 q + 16 cb + x at
+// TM + (16 q + x) * 4 + cb, so a lane's column in all four column blocks is
+// one 16-byte read.
+template <int TM>
 __device__ __forceinline__ int sw_slot(int c) {
-  return kTileM + (16 * (c >> 6) + (c & 15)) * 4 + ((c >> 4) & 3);
+  return TM + (16 * (c >> 6) + (c & 15)) * 4 + ((c >> 4) & 3);
 }
 
 __device__ __forceinline__ i32x8 lds_frag(const uint8_t* p0, const uint8_t* p1) {
@@ -97,10 +104,11 @@ struct LaneOffsets {
   int fw;         // packed weight chunk q4 of column wc + r16 (in a ring slot)
 };
 
+template <int TM>
 __device__ __forceinline__ LaneOffsets lane_offsets() {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, q4 = lane >> 4;
-  const int wr = (wave >> 2) * kWM, wc = (wave & 3) * kWN;
+  const int wr = (wave >> 2) * Geo<TM>::WM, wc = (wave & 3) * kWN;
   LaneOffsets o;
   o.fa0 = swz(wr + r16, 2 * q4);
   o.fa1 = swz(wr + r16, 2 * q4 + 1);
@@ -120,6 +128,16 @@ struct KBlock {
 
 __device__ __forceinline__ KBlock kblock(int e) { return KBlock{e & 1023, ((e >> 10) & 1) != 0, e >> 11}; }
 
+// The plan (schedule, work units, split table) is read-only while the kernel
+// runs.  Reading it through the constant address space keeps its loads on the
+// scalar unit: a vector load here would come with a wait on the vector-memory
+// counter, which also waits for every weight load in flight.
+typedef const __attribute__((address_space(4))) int* cint_ptr;
+__device__ __forceinline__ int plan_at(const int* a, int i) {
+  return ((cint_ptr)a)[i];
+}
+__device__ __forceinline__ int order_at(const GemmArgs& p, int i) { return plan_at(p.order, i); }
+
 // Registers holding one K-block's activation codes and a scale between load
 // and LDS store.
 struct Stage {
@@ -131,17 +149,19 @@ struct Stage {
 // (m0, n0).
 // Rows and columns are clamped into range, so edge tiles never read out of
 // bounds; clamped rows and columns compute values that are never stored.
+template <int TM>
 __device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, int m0, int n0,
                                            Stage& st) {
+  constexpr int N4 = TM / 128, N8 = TM / 64;  // 16-byte loads per lane, 4-bit / 8-bit block
   const int tid = threadIdx.x;
   const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)kb.aoff;
-  // 4-bit block: lane chunk tid%4 of rows tid/4 + 128 i (i < 2), 64 bytes a row;
-  // 8-bit block: lane chunk tid%8 of rows tid/8 + 64 i (i < 4), 128 bytes a row.
-  // The first two loads only switch offsets (arithmetic select, so that the
+  // 4-bit block: lane chunk tid%4 of rows tid/4 + 128 i (i < N4), 64 bytes a row;
+  // 8-bit block: lane chunk tid%8 of rows tid/8 + 64 i (i < N8), 128 bytes a row.
+  // The first N4 loads only switch offsets (arithmetic select, so that the
   // staging registers are not forced into memory by a branch merge).
   const uint32_t b8 = kb.b8 ? 1u : 0u;
   #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < N4; ++i) {
     const int r = b8 ? (tid >> 3) + 64 * i : (tid >> 2) + 128 * i;
     const uint32_t row = (uint32_t)min(m0 + r, p.M - 1);
     const uint32_t off = (row << (6 + b8)) + ((uint32_t)tid & (3u | (b8 << 2))) * 16u;
@@ -149,24 +169,26 @@ __device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, 
   }
   if (kb.b8) {
     #pragma unroll
-    for (int i = 2; i < 4; ++i) {
+    for (int i = N4; i < N8; ++i) {
       const uint32_t row = (uint32_t)min(m0 + (tid >> 3) + 64 * i, p.M - 1);
       st.a[i] = *reinterpret_cast<const u32x4*>(A + row * 128u + (tid & 7) * 16u);
     }
   }
-  if (tid < kTileM)
+  if (tid < TM)
     st.s = p.sa[(size_t)kb.g * p.M + min(m0 + tid, p.M - 1)];
   else
-    st.s = p.sw[(size_t)kb.g * p.N + min(n0 + tid - kTileM, p.N - 1)];
+    st.s = p.sw[(size_t)kb.g * p.N + min(n0 + min(tid - TM, kTileN - 1), p.N - 1)];
 }
 
+template <int TM>
 __device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* buf) {
+  constexpr int N4 = TM / 128, N8 = TM / 64;
   const int tid = threadIdx.x;
   const int st4a = swz(tid >> 2, 2 * (tid & 3)), st4b = swz(tid >> 2, 2 * (tid & 3) + 1);
   const int st8 = swz(tid >> 3, tid & 7);
   if (!b8) {
     #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < N4; ++i) {
       u32x4 lo, hi;
       unpack4(st.a[i], lo, hi);
       *reinterpret_cast<u32x4*>(buf + st4a + i * 16384) = lo;
@@ -174,14 +196,14 @@ __device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* b
     }
   } else {
     #pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + st8 + i * 8192) = st.a[i];
+    for (int i = 0; i < N8; ++i) *reinterpret_cast<u32x4*>(buf + st8 + i * 8192) = st.a[i];
   }
   const float f = __half2float(__ushort_as_half((unsigned short)st.s));
-  float* scales = reinterpret_cast<float*>(buf + kA);
-  if (tid < kTileM)
-    scales[sa_slot(tid)] = f * kUnit;
-  else
-    scales[sw_slot(tid - kTileM)] = f;
+  float* scales = reinterpret_cast<float*>(buf + Geo<TM>::A);
+  if (tid < TM)
+    scales[tid] = f * kUnit;
+  else if (tid < TM + kTileN)
+    scales[sw_slot<TM>(tid - TM)] = f;
 }
 
 // Direct global -> LDS load of 16 bytes per lane: the wave's 64 chunks land
@@ -231,19 +253,21 @@ __device__ __forceinline__ i32x8 unpack_frag(u32x4 v) {
 
 // One K-block of the wave's quadrant: activation stage `buf` (fp8 or raw
 // 8-bit codes, then scales), packed weights in ring slot `wbuf`.
-template <bool DIAG, bool B8>
+template <int TM, bool DIAG, bool B8>
 __device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t* wbuf,
                                               const LaneOffsets& o, int g, int NG, int m0, int n0,
-                                              const GemmArgs& p, f32x4 (&C)[kRB][kCB]) {
+                                              const GemmArgs& p,
+                                              f32x4 (&C)[Geo<TM>::RB][kCB]) {
+  constexpr int kRB = Geo<TM>::RB;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r16 = lane & 15, q4 = lane >> 4;
-  const int wr = (wave >> 2) * kWM;
+  const int wr = (wave >> 2) * Geo<TM>::WM;
   const int wc = (wave & 3) * kWN;
   // this lane's rows wr + 16 rb + 4 q4 + i (i < 4) and column wc + 16 cb + r16
-  const float* scales = reinterpret_cast<const float*>(buf + kA);
-  const float* sal = scales + ((wave >> 2) * 32 + q4) * 4;  // + 16 rb
-  const f32x4 swl = *reinterpret_cast<const f32x4*>(scales + kTileM + (16 * (wave & 3) + r16) * 4);
+  const float* scales = reinterpret_cast<const float*>(buf + Geo<TM>::A);
+  const float* sal = scales + wr + 4 * q4;  // + 16 rb
+  const f32x4 swl = *reinterpret_cast<const f32x4*>(scales + TM + (16 * (wave & 3) + r16) * 4);
 
   i32x8 wf[kCB];
   #pragma unroll
@@ -328,45 +352,50 @@ __device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t*
 // The weights of j + 1 were issued before this iteration's activation loads,
 // so they have arrived once those have (loads complete in order); the wait
 // before the barrier makes that explicit.
-template <bool DIAG, bool B8>
+template <int TM, bool DIAG, bool B8>
 __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o, uint8_t* smem,
                                       uint32_t lds, int g_begin, int pos, int end, int g_end,
-                                      int NG, int m0, int n0, Stage& st, f32x4 (&C)[kRB][kCB]) {
+                                      int NG, int m0, int n0, Stage& st,
+                                      f32x4 (&C)[Geo<TM>::RB][kCB]) {
+  constexpr int kBuf = Geo<TM>::Buf;
   for (; pos < end; ++pos) {
     const int j = pos - g_begin;
     const int cur = j & 1, wslot = j % 3;
     const bool more = pos + 1 < g_end;
-    const KBlock kb = kblock(p.order[pos]);
-    const KBlock kn = kblock(p.order[more ? pos + 1 : pos]);
-    if (more) stage_load(p, kn, m0, n0, st);
-    compute_block<DIAG, B8>(smem + cur * kBuf, smem + 2 * kBuf + wslot * kWr, o, kb.g, NG, m0,
-                            n0, p, C);
-    if (more) stage_store(st, kn.b8, smem + (cur ^ 1) * kBuf);
+    const KBlock kb = kblock(order_at(p, pos));
+    const KBlock kn = kblock(order_at(p, more ? pos + 1 : pos));
+    if (more) stage_load<TM>(p, kn, m0, n0, st);
+    compute_block<TM, DIAG, B8>(smem + cur * kBuf, smem + 2 * kBuf + wslot * kWr, o, kb.g, NG,
+                                m0, n0, p, C);
+    if (more) stage_store<TM>(st, kn.b8, smem + (cur ^ 1) * kBuf);
     wait_vm_all();
     if (pos + 2 < g_end) {
       const int nslot = wslot == 0 ? 2 : wslot - 1;  // (j + 2) % 3
-      dma_w(p, kblock(p.order[pos + 2]).g, n0, lds + 2 * kBuf + nslot * kWr);
+      dma_w(p, kblock(order_at(p, pos + 2)).g, n0, lds + 2 * kBuf + nslot * kWr);
     }
     barrier_lds();
   }
 }
 
-template <bool DIAG>
+template <int TM, bool DIAG>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
+  constexpr int kRB = Geo<TM>::RB, kBuf = Geo<TM>::Buf;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int s_last;
   const int NG = p.K / kG;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r16 = lane & 15, q4 = lane >> 4;
-  const LaneOffsets o = lane_offsets();
+  const LaneOffsets o = lane_offsets<TM>();
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
-  const int u_end = p.wg_begin[blockIdx.x + 1];
+  const int u_end = plan_at(p.wg_begin, blockIdx.x + 1);
 
-  for (int u = p.wg_begin[blockIdx.x]; u < u_end; ++u) {
-    const WorkUnit unit = p.units[u];
+  for (int u = plan_at(p.wg_begin, blockIdx.x); u < u_end; ++u) {
+    const int* ue = reinterpret_cast<const int*>(p.units) + 5 * u;
+    const WorkUnit unit{plan_at(ue, 0), plan_at(ue, 1), plan_at(ue, 2), plan_at(ue, 3),
+                        plan_at(ue, 4)};
     const int tm = unit.tile / p.tiles_n, tn = unit.tile % p.tiles_n;
-    const int m0 = tm * kTileM, n0 = tn * kTileN;
+    const int m0 = tm * TM, n0 = tn * kTileN;
 
     f32x4 C[kRB][kCB];
     #pragma unroll
@@ -377,26 +406,26 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
     // software pipeline over the unit's K-blocks; the schedule lists all
     // 4-bit blocks before the 8-bit ones, so each precision runs its own loop
     Stage st;
-    const KBlock k0 = kblock(p.order[unit.g_begin]);
+    const KBlock k0 = kblock(order_at(p, unit.g_begin));
     dma_w(p, k0.g, n0, lds + 2 * kBuf);
     if (unit.g_begin + 1 < unit.g_end)
-      dma_w(p, kblock(p.order[unit.g_begin + 1]).g, n0, lds + 2 * kBuf + kWr);
-    stage_load(p, k0, m0, n0, st);
-    stage_store(st, k0.b8, smem);
+      dma_w(p, kblock(order_at(p, unit.g_begin + 1)).g, n0, lds + 2 * kBuf + kWr);
+    stage_load<TM>(p, k0, m0, n0, st);
+    stage_store<TM>(st, k0.b8, smem);
     wait_vm_all();
     barrier_lds();
     const int split = min(max(p.n4, unit.g_begin), unit.g_end);
-    kloop<DIAG, false>(p, o, smem, lds, unit.g_begin, unit.g_begin, split, unit.g_end, NG, m0,
-                       n0, st, C);
-    kloop<DIAG, true>(p, o, smem, lds, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0, n0,
-                      st, C);
+    kloop<TM, DIAG, false>(p, o, smem, lds, unit.g_begin, unit.g_begin, split, unit.g_end, NG,
+                           m0, n0, st, C);
+    kloop<TM, DIAG, true>(p, o, smem, lds, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0,
+                          n0, st, C);
     if (DIAG) continue;
 
-    const int wr = (wave >> 2) * kWM, wc = (wave & 3) * kWN;
+    const int wr = (wave >> 2) * Geo<TM>::WM, wc = (wave & 3) * kWN;
     if (unit.nslots > 1) {
       // split tile: publish this slot's partial, then the last arriver reduces
-      const int base = p.split_index[unit.tile];
-      float* part = p.partials + (size_t)(base + unit.slot) * (kTileM * kTileN);
+      const int base = plan_at(p.split_index, unit.tile);
+      float* part = p.partials + (size_t)(base + unit.slot) * (TM * kTileN);
       #pragma unroll
       for (int rb = 0; rb < kRB; ++rb)
         #pragma unroll
@@ -414,7 +443,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
         #pragma unroll
         for (int cb = 0; cb < kCB; ++cb) C[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
       for (int s = 0; s < unit.nslots; ++s) {
-        const float* src = p.partials + (size_t)(base + s) * (kTileM * kTileN);
+        const float* src = p.partials + (size_t)(base + s) * (TM * kTileN);
         #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) {
           #pragma unroll
@@ -443,22 +472,36 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 
 }  // namespace
 
-int gemm_lds_bytes() { return kLds; }
+int gemm_lds_bytes(int tile_m) { return tile_m == 128 ? Geo<128>::Lds : Geo<256>::Lds; }
 
-hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, hipStream_t stream) {
-  if (diag)
-    hipLaunchKernelGGL(gemm_kernel<true>, dim3(num_wgs), dim3(kThreads), kLds, stream, a);
-  else
-    hipLaunchKernelGGL(gemm_kernel<false>, dim3(num_wgs), dim3(kThreads), kLds, stream, a);
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, int tile_m,
+                       hipStream_t stream) {
+  const dim3 grid(num_wgs), block(kThreads);
+  if (tile_m == 128) {
+    if (diag)
+      hipLaunchKernelGGL((gemm_kernel<128, true>), grid, block, Geo<128>::Lds, stream, a);
+    else
+      hipLaunchKernelGGL((gemm_kernel<128, false>), grid, block, Geo<128>::Lds, stream, a);
+  } else {
+    if (diag)
+      hipLaunchKernelGGL((gemm_kernel<256, true>), grid, block, Geo<256>::Lds, stream, a);
+    else
+      hipLaunchKernelGGL((gemm_kernel<256, false>), grid, block, Geo<256>::Lds, stream, a);
+  }
   return hipGetLastError();
 }
 
 hipError_t set_gemm_attributes() {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<false>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<true>),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+  const void* fns[4] = {reinterpret_cast<const void*>(&gemm_kernel<256, false>),
+                        reinterpret_cast<const void*>(&gemm_kernel<256, true>),
+                        reinterpret_cast<const void*>(&gemm_kernel<128, false>),
+                        reinterpret_cast<const void*>(&gemm_kernel<128, true>)};
+  const int lds[4] = {Geo<256>::Lds, Geo<256>::Lds, Geo<128>::Lds, Geo<128>::Lds};
+  for (int i = 0; i < 4; ++i) {
+    hipError_t e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, lds[i]);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace comet

@@ -65,12 +65,17 @@ hipError_t launch_kv4_quantize(const uint16_t* X, uint8_t* codes, uint16_t* para
 hipError_t launch_kv4_dequantize(const uint8_t* codes, const uint16_t* params, uint16_t* out,
                                  int T, int C, int G, hipStream_t stream);
 
-// Output tile of one GEMM workgroup.
+// Output tile of one GEMM workgroup: kTileN columns and kTileM rows, or
+// kTileMSmall rows when M <= kTileMSmall (a taller tile would leave MFMA rows
+// idle).
 constexpr int kTileM = 256;
+constexpr int kTileMSmall = 128;
 constexpr int kTileN = 256;
+inline int gemm_tile_m(int M) { return M <= kTileMSmall ? kTileMSmall : kTileM; }
 
-// Persistent GEMM: `num_wgs` workgroups walk a.units (a.wg_begin per group).
-hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, hipStream_t stream);
+// Persistent GEMM: `num_wgs` workgroups walk a.units (a.wg_begin per group);
+// tile_m is gemm_tile_m(a.M).
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, int tile_m, hipStream_t stream);
 // Few-token kernel (M <= kSkinnyMaxM): one wave per (16 columns, split-K slot).
 constexpr int kSkinnyMaxM = 64;
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
@@ -81,6 +86,6 @@ int skinny_splits(int N, int K, int cus);
 
 // Allows the GEMM's dynamic LDS size; once per process and device.
 hipError_t set_gemm_attributes();
-int gemm_lds_bytes();
+int gemm_lds_bytes(int tile_m);
 
 }  // namespace comet

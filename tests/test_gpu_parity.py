@@ -52,6 +52,10 @@ SHAPES = [
     (100, 272, 1152, "random"),
     (257, 400, 640, "alternate"),
     (130, 144, 384, "cfg0"),
+    # 128-row tiles (64 < M <= 128): ragged rows and columns, both precisions
+    (65, 528, 640, "alternate"),
+    (128, 784, 1024, "all8"),
+    (97, 4096, 2048, "random"),
 ]
 
 
@@ -194,3 +198,17 @@ def test_llama3_70b_decode_full_size(M):
     qw, sw = oracle.quantize_weight(r["W16"])
     ref = oracle.dequant_gemm(qa, sa, qw, sw)
     assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"decode M={M}")
+
+
+@pytest.mark.parametrize("M", [96, 128])
+def test_llama3_70b_decode_128_row_tiles_sampled_rows(M):
+    # LLaMA-3-70B gate_up with 128-row tiles; a sample of rows on both halves
+    # of the tile checked against the oracle
+    K, N = synth.LLAMA3_70B["gate_up"]
+    prec = synth.prec_map(K // 128, K // 128 // 16)
+    r = run_path(M, N, K, prec, seed=M)
+    rows = np.array([0, 1, 63, 64, M - 1])
+    qa, sa = oracle.quantize_act(r["X16"][rows], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16)[rows], ref, f"decode M={M}")

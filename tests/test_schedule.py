@@ -84,3 +84,11 @@ def test_small_cu_counts():
     prec = synth.prec_map(8, 1)
     for cus in (1, 3, 7, 64):
         check_plan(300, 1024, 1024, prec, num_cus=cus)
+
+
+def test_tile_height_follows_m():
+    # the tile kernel uses 128-row tiles up to M = 128 and 256-row tiles above
+    prec = np.full(64, 4, np.uint8)
+    for M, want in ((65, 128), (100, 128), (128, 128), (129, 256), (4096, 256)):
+        s = comet.comet_schedule_query(M, 57344, 8192, prec)
+        assert s["tile_m"] == want and s["tile_n"] == 256
