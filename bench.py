@@ -54,9 +54,11 @@ CSRC = os.path.join(ROOT, "paper_2410_12168_amd", "csrc")
 KERNEL_SOURCES = {
     "tile": ["gemm.hip", "operand.h", "kernels.h"],
     "skinny": ["gemm_skinny.hip", "operand.h", "kernels.h"],
+    "mid": ["gemm.hip", "operand.h", "kernels.h"],
     "kv4": ["kv4.hip"],
 }
-SKINNY_MAX_M = 64  # the library runs the few-token kernel up to this M
+SKINNY_MAX_M = 48  # the library runs the few-token kernel up to this M,
+MID_MAX_M = 128    # and the 128-row-tile kernel up to this one
 
 
 def kernel_sha(kind: str) -> str:
@@ -254,7 +256,7 @@ def main():
     # the dominant kernel launch: the GEMM of the layer with the most work
     d = int(np.argmax(ops))
     D = layers[d]
-    kind = "skinny" if M <= SKINNY_MAX_M else "tile"
+    kind = "skinny" if M <= SKINNY_MAX_M else ("mid" if M <= MID_MAX_M else "tile")
     if hbm_bound:
         achieved = float(gbytes[d] / (g_ms[d] * 1e-3) / 1e9)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,

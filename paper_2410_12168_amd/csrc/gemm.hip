@@ -251,10 +251,20 @@ __device__ __forceinline__ i32x8 unpack_frag(u32x4 v) {
   return f;
 }
 
+// The lane's weight scales (column wc + 16 cb + r16, cb < 4) from an
+// activation stage's fp32 scale table.
+template <int TM>
+__device__ __forceinline__ f32x4 stage_sw(const uint8_t* buf) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float* scales = reinterpret_cast<const float*>(buf + Geo<TM>::A);
+  return *reinterpret_cast<const f32x4*>(scales + TM + (16 * (wave & 3) + (lane & 15)) * 4);
+}
+
 // One K-block of the wave's quadrant: activation stage `buf` (fp8 or raw
-// 8-bit codes, then scales), packed weights in ring slot `wbuf`.
+// 8-bit codes, then activation scales), packed weights in ring slot `wbuf`,
+// the lane's weight scales in swl.
 template <int TM, bool DIAG, bool B8>
-__device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t* wbuf,
+__device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t* wbuf, f32x4 swl,
                                               const LaneOffsets& o, int g, int NG, int m0, int n0,
                                               const GemmArgs& p,
                                               f32x4 (&C)[Geo<TM>::RB][kCB]) {
@@ -267,7 +277,6 @@ __device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t*
   // this lane's rows wr + 16 rb + 4 q4 + i (i < 4) and column wc + 16 cb + r16
   const float* scales = reinterpret_cast<const float*>(buf + Geo<TM>::A);
   const float* sal = scales + wr + 4 * q4;  // + 16 rb
-  const f32x4 swl = *reinterpret_cast<const f32x4*>(scales + TM + (16 * (wave & 3) + r16) * 4);
 
   i32x8 wf[kCB];
   #pragma unroll
@@ -365,8 +374,8 @@ __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o, u
     const KBlock kb = kblock(order_at(p, pos));
     const KBlock kn = kblock(order_at(p, more ? pos + 1 : pos));
     if (more) stage_load<TM>(p, kn, m0, n0, st);
-    compute_block<TM, DIAG, B8>(smem + cur * kBuf, smem + 2 * kBuf + wslot * kWr, o, kb.g, NG,
-                                m0, n0, p, C);
+    compute_block<TM, DIAG, B8>(smem + cur * kBuf, smem + 2 * kBuf + wslot * kWr,
+                                stage_sw<TM>(smem + cur * kBuf), o, kb.g, NG, m0, n0, p, C);
     if (more) stage_store<TM>(st, kn.b8, smem + (cur ^ 1) * kBuf);
     wait_vm_all();
     if (pos + 2 < g_end) {
@@ -377,15 +386,77 @@ __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o, u
   }
 }
 
+// Epilogue of a work unit: a whole tile is stored as fp16; a split tile
+// publishes this slot's fp32 partial, and the last workgroup to arrive adds
+// the partials in slot order and stores fp16.
+template <int TM>
+__device__ __forceinline__ void store_tile(const GemmArgs& p, const WorkUnit& unit, int m0, int n0,
+                                           f32x4 (&C)[Geo<TM>::RB][kCB], int* s_last) {
+  constexpr int kRB = Geo<TM>::RB;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const int wr = (wave >> 2) * Geo<TM>::WM, wc = (wave & 3) * kWN;
+  if (unit.nslots > 1) {
+    // split tile: publish this slot's partial, then the last arriver reduces
+    const int base = plan_at(p.split_index, unit.tile);
+    float* part = p.partials + (size_t)(base + unit.slot) * (TM * kTileN);
+    #pragma unroll
+    for (int rb = 0; rb < kRB; ++rb)
+      #pragma unroll
+      for (int cb = 0; cb < kCB; ++cb)
+        *reinterpret_cast<f32x4*>(part + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4) =
+            C[rb][cb];
+    // One device-scope release and one acquire per tile slot, by one
+    // thread: on this multi-XCD part each is a write-back or invalidate of
+    // the whole L2, too costly to issue from every wave.  The barrier first
+    // completes every wave's partial stores into L2.
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __threadfence();
+      const bool last = atomicAdd(p.counters + base, 1) == unit.nslots - 1;
+      if (last) __threadfence();
+      *s_last = last;
+    }
+    __syncthreads();
+    if (!*s_last) return;
+    #pragma unroll
+    for (int rb = 0; rb < kRB; ++rb)
+      #pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) C[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < unit.nslots; ++s) {
+      const float* src = p.partials + (size_t)(base + s) * (TM * kTileN);
+      #pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) {
+        #pragma unroll
+        for (int cb = 0; cb < kCB; ++cb)
+          C[rb][cb] += *reinterpret_cast<const f32x4*>(
+              src + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if (threadIdx.x == 0) p.counters[base] = 0;  // ready for the next launch
+  }
+  #pragma unroll
+  for (int rb = 0; rb < kRB; ++rb)
+    #pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) {
+      const int col = n0 + wc + cb * 16 + r16;
+      #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + wr + rb * 16 + 4 * q4 + i;
+        if (row < p.M && col < p.N)
+          p.out[(size_t)row * p.N + col] = __half_as_ushort(__float2half_rn(C[rb][cb][i]));
+      }
+    }
+}
+
 template <int TM, bool DIAG>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
   constexpr int kRB = Geo<TM>::RB, kBuf = Geo<TM>::Buf;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int s_last;
   const int NG = p.K / kG;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, q4 = lane >> 4;
   const LaneOffsets o = lane_offsets<TM>();
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
   const int u_end = plan_at(p.wg_begin, blockIdx.x + 1);
@@ -421,67 +492,207 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
                           n0, st, C);
     if (DIAG) continue;
 
-    const int wr = (wave >> 2) * Geo<TM>::WM, wc = (wave & 3) * kWN;
-    if (unit.nslots > 1) {
-      // split tile: publish this slot's partial, then the last arriver reduces
-      const int base = plan_at(p.split_index, unit.tile);
-      float* part = p.partials + (size_t)(base + unit.slot) * (TM * kTileN);
-      #pragma unroll
-      for (int rb = 0; rb < kRB; ++rb)
-        #pragma unroll
-        for (int cb = 0; cb < kCB; ++cb)
-          *reinterpret_cast<f32x4*>(part + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4) =
-              C[rb][cb];
-      __threadfence();
-      __syncthreads();
-      if (threadIdx.x == 0) s_last = atomicAdd(p.counters + base, 1) == unit.nslots - 1;
-      __syncthreads();
-      if (!s_last) continue;
-      __threadfence();
-      #pragma unroll
-      for (int rb = 0; rb < kRB; ++rb)
-        #pragma unroll
-        for (int cb = 0; cb < kCB; ++cb) C[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < unit.nslots; ++s) {
-        const float* src = p.partials + (size_t)(base + s) * (TM * kTileN);
-        #pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) {
-          #pragma unroll
-          for (int cb = 0; cb < kCB; ++cb)
-            C[rb][cb] += *reinterpret_cast<const f32x4*>(
-                src + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
-      if (threadIdx.x == 0) p.counters[base] = 0;  // ready for the next launch
-    }
+    store_tile<TM>(p, unit, m0, n0, C, &s_last);
+  }
+}
+
+
+// ---------------------------------------------------------------------------
+// Mid-size GEMM (64 < M <= 128): 128-row tiles, with the workgroup's waves
+// split by role so that no load is waited for early.  With this few rows the
+// weights come from HBM exactly once and a K-block computes briefly, so the
+// loads need several K-blocks of lead, and a wait on the vector-memory counter
+// covers every older load of the wave:
+//   * waves 0-3 only issue direct loads: a K-block's packed weights and its
+//     fp16 weight scales, into a ring of four slots three K-blocks ahead, and
+//     wait for them with counted waits;
+//   * waves 4-7 stage the activation codes and scales (few rows, written just
+//     before by the quantizer, so they come from L2) through registers one
+//     K-block ahead, unpack 4-bit codes once and store them to a
+//     double-buffered LDS stage;
+//   * all eight waves compute their 64 x 64 quadrant with the tile kernel's
+//     K-block step.
+constexpr int kMidTM = 128;
+constexpr int kMidD = 4;                                // weight ring slots
+constexpr int kMidSlot = kWr + 2 * kTileN;              // packed weights + fp16 weight scales
+constexpr int kMidStage = Geo<kMidTM>::A + 4 * kMidTM;  // codes + fp32 activation scales
+constexpr int kMidLds = 2 * kMidStage + kMidD * kMidSlot;
+constexpr int kMidVm = 5;  // direct loads per K-block and weight wave
+
+// Waves 0-3: packed weights of K-block g (16 KB, four 1 KB loads per wave, in
+// the ring layout of dma_w) and the fp16 scales of the slot's 256 columns
+// (lanes 0-7 of each wave: columns n0 + 64 wave + 8 lane .. + 7, at byte
+// kWr + 2 * (column - n0)).  Columns past N re-read the last valid ones.
+__device__ __forceinline__ void mid_dma(const GemmArgs& p, int g, int n0, uint32_t slot) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
+  #pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = 4 * wave + i;
+    const uint32_t col = (uint32_t)min(n0 + 16 * j + (lane >> 2), p.N - 1);
+    const uint8_t* src = p.W + (size_t)col * (uint32_t)(p.K / 2) + (size_t)g * 64 + chunk * 16;
+    dma16(src, slot + j * 1024);
+  }
+  const int c0 = min(n0 + 64 * wave + 8 * (lane & 7), p.N - 8);
+  if (lane < 8) dma16(p.sw + (size_t)g * p.N + c0, slot + kWr + 128 * wave);
+}
+
+// Wait until at most n of this wave's direct loads are in flight (n = 0, 5
+// or 10: the loads of the next zero, one or two K-blocks).
+__device__ __forceinline__ void mid_wait(int n) {
+  if (n >= 2 * kMidVm)
+    asm volatile("s_waitcnt vmcnt(10)" ::: "memory");
+  else if (n >= kMidVm)
+    asm volatile("s_waitcnt vmcnt(5)" ::: "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// The lane's weight scales (column wc + 16 cb + r16, cb < 4) from a ring slot.
+__device__ __forceinline__ f32x4 slot_sw(const uint8_t* slot) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint16_t* sw =
+      reinterpret_cast<const uint16_t*>(slot + kWr) + 64 * (wave & 3) + (lane & 15);
+  return f32x4{__half2float(__ushort_as_half(sw[0])), __half2float(__ushort_as_half(sw[16])),
+               __half2float(__ushort_as_half(sw[32])), __half2float(__ushort_as_half(sw[48]))};
+}
+
+// Waves 4-7 (t = threadIdx.x - 256): one K-block's activation codes and scale.
+// 4-bit block: chunk t % 4 of rows t / 4 + 64 i (i < 2); 8-bit block: chunk
+// t % 8 of rows t / 8 + 32 i (i < 4).  Rows past M are clamped.
+__device__ __forceinline__ void mid_load(const GemmArgs& p, const KBlock& kb, int m0, Stage& st) {
+  const int t = threadIdx.x - 256;
+  const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)kb.aoff;
+  const uint32_t b8 = kb.b8 ? 1u : 0u;
+  #pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = b8 ? (t >> 3) + 32 * i : (t >> 2) + 64 * i;
+    const uint32_t row = (uint32_t)min(m0 + r, p.M - 1);
+    const uint32_t off = (row << (6 + b8)) + ((uint32_t)t & (3u | (b8 << 2))) * 16u;
+    st.a[i] = *reinterpret_cast<const u32x4*>(A + off);
+  }
+  if (kb.b8) {
     #pragma unroll
-    for (int rb = 0; rb < kRB; ++rb)
+    for (int i = 2; i < 4; ++i) {
+      const uint32_t row = (uint32_t)min(m0 + (t >> 3) + 32 * i, p.M - 1);
+      st.a[i] = *reinterpret_cast<const u32x4*>(A + row * 128u + (t & 7) * 16u);
+    }
+  }
+  st.s = p.sa[(size_t)kb.g * p.M + min(m0 + (t & (kMidTM - 1)), p.M - 1)];
+}
+
+__device__ __forceinline__ void mid_store(const Stage& st, bool b8, uint8_t* buf) {
+  const int t = threadIdx.x - 256;
+  if (!b8) {
+    const int r = t >> 2, c = t & 3;
+    #pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      u32x4 lo, hi;
+      unpack4(st.a[i], lo, hi);
+      *reinterpret_cast<u32x4*>(buf + swz(r, 2 * c) + i * 8192) = lo;
+      *reinterpret_cast<u32x4*>(buf + swz(r, 2 * c + 1) + i * 8192) = hi;
+    }
+  } else {
+    const int off = swz(t >> 3, t & 7);
+    #pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + off + i * 4096) = st.a[i];
+  }
+  if (t < kMidTM)
+    reinterpret_cast<float*>(buf + Geo<kMidTM>::A)[t] =
+        __half2float(__ushort_as_half((unsigned short)st.s)) * kUnit;
+}
+
+// One K-block position of the mid-size loop: weights of pos + 3 issued,
+// activations of pos + 1 loaded and stored to the other stage.
+template <bool DIAG, bool B8>
+__device__ __forceinline__ void mid_loop(const GemmArgs& p, const LaneOffsets& o, uint8_t* smem,
+                                         uint32_t lds, int pos, int end, int gb, int ge, int NG,
+                                         int m0, int n0, Stage& st,
+                                         f32x4 (&C)[Geo<kMidTM>::RB][kCB]) {
+  const bool wwave = threadIdx.x < 256;
+  for (; pos < end; ++pos) {
+    const int j = pos - gb;
+    const KBlock kb = kblock(order_at(p, pos));
+    const bool more = pos + 1 < ge;
+    const KBlock kn = kblock(order_at(p, more ? pos + 1 : pos));
+    const uint8_t* slot = smem + 2 * kMidStage + (j & 3) * kMidSlot;
+    if (wwave) {
+      if (pos + 3 < ge)
+        mid_dma(p, kblock(order_at(p, pos + 3)).g, n0,
+                lds + 2 * kMidStage + ((j + 3) & 3) * kMidSlot);
+    } else if (more) {
+      mid_load(p, kn, m0, st);
+    }
+    compute_block<kMidTM, DIAG, B8>(smem + (j & 1) * kMidStage, slot, slot_sw(slot), o, kb.g, NG,
+                                    m0, n0, p, C);
+    if (wwave)
+      mid_wait(kMidVm * min(max(ge - pos - 2, 0), 2));
+    else if (more)
+      mid_store(st, kn.b8, smem + ((j + 1) & 1) * kMidStage);
+    barrier_lds();
+  }
+}
+
+template <bool DIAG>
+__global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
+  constexpr int TM = kMidTM, kRB = Geo<TM>::RB;
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  __shared__ int s_last;
+  const int NG = p.K / kG;
+  const LaneOffsets o = lane_offsets<TM>();
+  const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
+  const bool wwave = threadIdx.x < 256;
+  const int u_end = plan_at(p.wg_begin, blockIdx.x + 1);
+
+  for (int u = plan_at(p.wg_begin, blockIdx.x); u < u_end; ++u) {
+    const int* ue = reinterpret_cast<const int*>(p.units) + 5 * u;
+    const WorkUnit unit{plan_at(ue, 0), plan_at(ue, 1), plan_at(ue, 2), plan_at(ue, 3),
+                        plan_at(ue, 4)};
+    const int tm = unit.tile / p.tiles_n, tn = unit.tile % p.tiles_n;
+    const int m0 = tm * TM, n0 = tn * kTileN;
+    const int gb = unit.g_begin, ge = unit.g_end;
+
+    f32x4 C[kRB][kCB];
+    #pragma unroll
+    for (int i = 0; i < kRB; ++i)
       #pragma unroll
-      for (int cb = 0; cb < kCB; ++cb) {
-        const int col = n0 + wc + cb * 16 + r16;
-        #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = m0 + wr + rb * 16 + 4 * q4 + i;
-          if (row < p.M && col < p.N)
-            p.out[(size_t)row * p.N + col] = __half_as_ushort(__float2half_rn(C[rb][cb][i]));
-        }
-      }
+      for (int j = 0; j < kCB; ++j) C[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // prologue: weights of the first three K-blocks in flight, activations
+    // of the first stored
+    Stage st;
+    if (wwave) {
+      for (int d = 0; d < 3 && gb + d < ge; ++d)
+        mid_dma(p, kblock(order_at(p, gb + d)).g, n0, lds + 2 * kMidStage + d * kMidSlot);
+      mid_wait(kMidVm * min(ge - gb - 1, 2));
+    } else {
+      const KBlock k0 = kblock(order_at(p, gb));
+      mid_load(p, k0, m0, st);
+      mid_store(st, k0.b8, smem);
+    }
+    barrier_lds();
+    const int split = min(max(p.n4, gb), ge);
+    mid_loop<DIAG, false>(p, o, smem, lds, gb, split, gb, ge, NG, m0, n0, st, C);
+    mid_loop<DIAG, true>(p, o, smem, lds, split, ge, gb, ge, NG, m0, n0, st, C);
+    if (DIAG) continue;
+
+    store_tile<TM>(p, unit, m0, n0, C, &s_last);
   }
 }
 
 }  // namespace
 
-int gemm_lds_bytes(int tile_m) { return tile_m == 128 ? Geo<128>::Lds : Geo<256>::Lds; }
+int gemm_lds_bytes(int tile_m) { return tile_m == kMidTM ? kMidLds : Geo<256>::Lds; }
 
 hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, int tile_m,
                        hipStream_t stream) {
   const dim3 grid(num_wgs), block(kThreads);
-  if (tile_m == 128) {
+  if (tile_m == kMidTM) {
     if (diag)
-      hipLaunchKernelGGL((gemm_kernel<128, true>), grid, block, Geo<128>::Lds, stream, a);
+      hipLaunchKernelGGL(gemm_mid_kernel<true>, grid, block, kMidLds, stream, a);
     else
-      hipLaunchKernelGGL((gemm_kernel<128, false>), grid, block, Geo<128>::Lds, stream, a);
+      hipLaunchKernelGGL(gemm_mid_kernel<false>, grid, block, kMidLds, stream, a);
   } else {
     if (diag)
       hipLaunchKernelGGL((gemm_kernel<256, true>), grid, block, Geo<256>::Lds, stream, a);
@@ -494,9 +705,9 @@ hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, int tile_m,
 hipError_t set_gemm_attributes() {
   const void* fns[4] = {reinterpret_cast<const void*>(&gemm_kernel<256, false>),
                         reinterpret_cast<const void*>(&gemm_kernel<256, true>),
-                        reinterpret_cast<const void*>(&gemm_kernel<128, false>),
-                        reinterpret_cast<const void*>(&gemm_kernel<128, true>)};
-  const int lds[4] = {Geo<256>::Lds, Geo<256>::Lds, Geo<128>::Lds, Geo<128>::Lds};
+                        reinterpret_cast<const void*>(&gemm_mid_kernel<false>),
+                        reinterpret_cast<const void*>(&gemm_mid_kernel<true>)};
+  const int lds[4] = {Geo<256>::Lds, Geo<256>::Lds, kMidLds, kMidLds};
   for (int i = 0; i < 4; ++i) {
     hipError_t e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, lds[i]);
     if (e != hipSuccess) return e;

@@ -1,7 +1,7 @@
-// gemm_skinny.hip -- W4Ax GEMM for few tokens (decode, M <= 64) on gfx950.
+// gemm_skinny.hip -- W4Ax GEMM for few tokens (decode, M <= 48) on gfx950.
 //
 // With a handful of tokens the GEMM is a weight stream: every 4-bit weight is
-// read from HBM once and used by at most 64 activation rows, so the bound is
+// read from HBM once and used by at most 48 activation rows, so the bound is
 // HBM bandwidth, not the matrix cores.  Each wave owns 16 output columns and
 // a contiguous K-block range (split-K slot), walked in natural block order in
 // batches of four K-blocks.  A batch's weights are 256 contiguous bytes of
@@ -308,7 +308,6 @@ hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream) 
     case 1: return launch_r<1>(a, diag, stream);
     case 2: return launch_r<2>(a, diag, stream);
     case 3: return launch_r<3>(a, diag, stream);
-    case 4: return launch_r<4>(a, diag, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -77,7 +77,7 @@ inline int gemm_tile_m(int M) { return M <= kTileMSmall ? kTileMSmall : kTileM; 
 // tile_m is gemm_tile_m(a.M).
 hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, int tile_m, hipStream_t stream);
 // Few-token kernel (M <= kSkinnyMaxM): one wave per (16 columns, split-K slot).
-constexpr int kSkinnyMaxM = 64;
+constexpr int kSkinnyMaxM = 48;
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
 // Split-K slots (1, 2 or 4) for the few-token kernel: spread the (N/16 x
 // slots) waves evenly over the device's SIMDs, keeping at least 4 K-blocks per

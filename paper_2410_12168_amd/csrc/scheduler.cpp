@@ -76,11 +76,19 @@ bool build_plan(int M, int N, int K, int G, const uint8_t* prec, const PlanOptio
   const std::vector<int> seq = tile_sequence(p.tiles_m, p.tiles_n);
   p.split_base.assign(T, -1);
 
-  // How many tiles go to data-parallel waves, and how many are split.
+  // How many tiles go to data-parallel waves, and how many are split.  A
+  // split tile costs a fixup (fp32 partials, and a device-scope release and
+  // acquire, each a whole-L2 write-back or invalidate on a multi-XCD part),
+  // measured at about a quarter to a third of a wave of tiles.  So the last
+  // wave is split only when, unsplit, it would leave a larger share of the
+  // workgroups idle.
   int dp_tiles = T;
   if (opt.mode == "cost" && T % P != 0) {
-    const int full = T / P;
-    dp_tiles = full >= 1 ? (full - 1) * P : 0;
+    const double idle = (double)(P - T % P) / P;
+    if (idle > opt.split_min_idle) {
+      const int full = T / P;
+      dp_tiles = full >= 1 ? (full - 1) * P : 0;
+    }
   } else if (opt.mode != "dp" && opt.mode != "cost") {
     if (err) *err = "build_plan: unknown mode " + opt.mode;
     return false;

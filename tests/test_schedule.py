@@ -92,3 +92,16 @@ def test_tile_height_follows_m():
     for M, want in ((65, 128), (100, 128), (128, 128), (129, 256), (4096, 256)):
         s = comet.comet_schedule_query(M, 57344, 8192, prec)
         assert s["tile_m"] == want and s["tile_n"] == 256
+
+
+@pytest.mark.parametrize("M,N,split", [(128, 57344, False),   # 224 tiles: 12.5% of a wave idle
+                                       (4096, 7936, False),   # 496 tiles: 6% idle
+                                       (4096, 10240, True),   # 640 tiles: half a wave idle
+                                       (2048, 28672, True)])  # 896 tiles
+def test_last_wave_split_only_when_worth_it(M, N, split):
+    # a split tile costs a cross-workgroup fixup; the last wave is split only
+    # when leaving it whole would idle more than 30% of the workgroups
+    K = 8192
+    prec = synth.prec_map(K // 128, 4)
+    s, wg_cost, Ct = check_plan(M, N, K, prec)
+    assert bool((s["units"][:, 4] > 1).any()) == split
