@@ -28,8 +28,12 @@
  *     8-bit chunk (G = 128 bytes): byte c = (sign << 7) | |code c|.
  *   - A_packed: block-major.  Block g starts at byte M * sum_{g'<g} B(p[g']),
  *     B(4) = 64, B(8) = 128; row m of block g follows at + m * B(p[g]).
- *   - a_scales: fp16 [K/G][M];  W_packed: [N][K/2] row-major, row n block g at
- *     byte n*K/2 + 64*g;  w_scales: fp16 [K/G][N];  out: fp16 [M][N] row-major.
+ *   - a_scales: fp16 [K/G][M];  w_scales: fp16 [K/G][N];  out: fp16 [M][N]
+ *     row-major.
+ *   - W_packed: N*K/2 bytes in 16-row panels (N a multiple of 16): row n's
+ *     block g at byte ((n/16 * K/G + g) * 16 + n % 16) * 64, so the 16 rows of
+ *     a panel hold each block in one contiguous kilobyte (Sec. 4.3: a weight
+ *     layout made for the kernel's loads).
  *
  * Conventions for every call:
  *   - Device pointers are caller-owned HIP device allocations on the current
@@ -96,8 +100,8 @@ COMET_API comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_
 
 /* Offline 4-bit weight quantization and packing (weights are 4-bit, Sec. 3.2;
  * stored in the operand layout the GEMM reads, Sec. 4.3).
- *   W        device, fp16 [N][K] row-major (nn.Linear layout).
- *   W_packed device, [N][K/2] bytes.
+ *   W        device, fp16 [N][K] row-major (nn.Linear layout); N a multiple of 16.
+ *   W_packed device, N*K/2 bytes in 16-row panels (see above).
  *   w_scales device, fp16 [K/G][N]. */
 COMET_API comet_status_t comet_pack_w4(const uint16_t* W, uint8_t* W_packed, uint16_t* w_scales, int N,
                              int K, int G, hipStream_t stream);

@@ -154,6 +154,7 @@ def pack_act(qa, prec, G: int = 128) -> np.ndarray:
 
 
 def pack_weight(qw, G: int = 128) -> np.ndarray:
+    """N*K/2 bytes in 16-row panels (see oracle.h), returned with shape (N, K/2)."""
     qw = _c(qw, np.int8)
     N, K = qw.shape
     out = np.empty((N, K // 2), dtype=np.uint8)

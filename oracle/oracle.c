@@ -205,11 +205,14 @@ int orc_pack_act(const int8_t* qa, const uint8_t* prec, int M, int K, int G, uin
 }
 
 int orc_pack_weight(const int8_t* qw, int N, int K, int G, uint8_t* W_packed) {
-  if (N < 0 || K <= 0 || G <= 0 || K % G || G % 8) return -1;
+  if (N < 0 || N % 16 || K <= 0 || G <= 0 || K % G || G % 8) return -1;
+  const int NG = K / G;
   for (int n = 0; n < N; ++n)
-    for (int g = 0; g < K / G; ++g)
-      orc_encode4(qw + (size_t)n * K + (size_t)g * G, G,
-                  W_packed + (size_t)n * (K / 2) + (size_t)g * (G / 2));
+    for (int g = 0; g < NG; ++g) {
+      /* 16-row panel n / 16, block g, row n % 16 */
+      const size_t chunk = ((size_t)(n / 16) * NG + g) * 16 + (size_t)(n % 16);
+      orc_encode4(qw + (size_t)n * K + (size_t)g * G, G, W_packed + chunk * (G / 2));
+    }
   return 0;
 }
 

@@ -34,7 +34,9 @@
  *   An 8-bit chunk holds G bytes, byte c = (s[c] << 7) | m[c], m = 0..127.
  *   A_packed: block-major.  Block g starts at byte M * sum_{g'<g} B(p[g']),
  *             B(4) = G/2, B(8) = G; row m of block g follows at + m * B(p[g]).
- *   W_packed: row-major [N][K/2]; row n, block g at byte n*K/2 + g*G/2.
+ *   W_packed: 16-row panels, N a multiple of 16: row n, block g at byte
+ *             ((n/16 * K/G + g) * 16 + n % 16) * G/2, so the 16 rows of a panel
+ *             hold each block in 16*G/2 contiguous bytes.
  *   a_scales: fp16 [K/G][M]; w_scales: fp16 [K/G][N].
  */
 #ifndef COMET_ORACLE_H

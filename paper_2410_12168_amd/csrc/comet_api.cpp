@@ -380,7 +380,8 @@ comet_status_t comet_fmpq_quantize_act(const uint16_t* X, const uint8_t* prec, u
 comet_status_t comet_pack_w4_perm(const uint16_t* W, const int32_t* perm, uint8_t* W_packed,
                                   uint16_t* w_scales, int N, int K, int G, hipStream_t stream) {
   if (!W || !W_packed || !w_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
-  if (N < 1) return fail(COMET_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+  if (N < 16 || N % 16)
+    return fail(COMET_ERR_INVALID_ARG, "N=%d must be a positive multiple of 16", N);
   comet_status_t st = check_kg(K, G);
   if (st) return st;
   if (!aligned16(W) || !aligned16(W_packed) || !aligned16(w_scales) || !aligned16(perm))

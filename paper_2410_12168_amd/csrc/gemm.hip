@@ -215,20 +215,27 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
                :: "v"(g), "s"(lds) : "memory", "m0");
 }
 
-// Packed weights of K-block g for the tile's 256 columns into a ring slot:
-// 16 KB, two 1 KB wave loads per wave.  Lane L of load j fills column
-// 16 j + L / 4, slot L % 4, with the chunk that wswz() places there.
-// Columns past N are clamped (their outputs are never stored).
-__device__ __forceinline__ void dma_w(const GemmArgs& p, int g, int n0, uint32_t slot) {
+// Source of one 1 KB wave load of packed weights: K-block g of the 16-column
+// panel j of the tile at n0 (one contiguous kilobyte of W_packed).  Lane L
+// fills column 16 j + L / 4, slot L % 4 of the ring layout with the chunk
+// that wswz() places there.  Panels past N are clamped (their outputs are
+// never stored).
+__device__ __forceinline__ const uint8_t* w_src(const GemmArgs& p, int g, int n0, int j) {
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int NG = p.K / kG;
+  const int panel = min(n0 / 16 + j, p.N / 16 - 1);
   const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
+  return p.W + ((size_t)panel * NG + g) * 1024 + (lane >> 2) * 64 + chunk * 16;
+}
+
+// Packed weights of K-block g for the tile's 256 columns into a ring slot:
+// 16 KB, two 1 KB wave loads per wave.
+__device__ __forceinline__ void dma_w(const GemmArgs& p, int g, int n0, uint32_t slot) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int j = 2 * wave + i;
-    const uint32_t col = (uint32_t)min(n0 + 16 * j + (lane >> 2), p.N - 1);
-    const uint8_t* src = p.W + (size_t)col * (uint32_t)(p.K / 2) + (size_t)g * 64 + chunk * 16;
-    dma16(src, slot + j * 1024);
+    dma16(w_src(p, g, n0, j), slot + j * 1024);
   }
 }
 
@@ -526,13 +533,10 @@ constexpr int kMidVm = 5;  // direct loads per K-block and weight wave
 __device__ __forceinline__ void mid_dma(const GemmArgs& p, int g, int n0, uint32_t slot) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
   #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int j = 4 * wave + i;
-    const uint32_t col = (uint32_t)min(n0 + 16 * j + (lane >> 2), p.N - 1);
-    const uint8_t* src = p.W + (size_t)col * (uint32_t)(p.K / 2) + (size_t)g * 64 + chunk * 16;
-    dma16(src, slot + j * 1024);
+    dma16(w_src(p, g, n0, j), slot + j * 1024);
   }
   const int c0 = min(n0 + 64 * wave + 8 * (lane & 7), p.N - 8);
   if (lane < 8) dma16(p.sw + (size_t)g * p.N + c0, slot + kWr + 128 * wave);

@@ -4,15 +4,13 @@
 // read from HBM once and used by at most 48 activation rows, so the bound is
 // HBM bandwidth, not the matrix cores.  Each wave owns 16 output columns and
 // a contiguous K-block range (split-K slot), walked in natural block order in
-// batches of four K-blocks.  A batch's weights are 256 contiguous bytes of
-// each of the wave's 16 weight rows: four nontemporal 128-bit loads per lane,
-// each covering 4 rows x 256 bytes (whole cache lines, long runs per row: the
-// fastest read shape measured on MI355X for this layout).  The next batch is
-// in flight while the current one computes.  The wave rearranges each batch
-// into MFMA fragments through a private 4 KB LDS buffer (write as loaded,
-// read per K-block, XOR-swizzled so both sides are bank-conflict free), so
-// no lane shuffles cost vector-ALU time.  The tiny activation operand and
-// the scales are read through L2, one K-block ahead.
+// batches of four K-blocks.  The wave's 16 weight rows are one panel of
+// W_packed, where each K-block is one contiguous kilobyte: one nontemporal
+// 128-bit load per lane and K-block reads it whole, and lane r + 16 q lands
+// exactly on its MFMA fragment (row r, codes 32 q .. 32 q + 31), so the
+// weights go from HBM to the matrix core with no LDS round trip.  The next
+// batch is in flight while the current one computes.  The tiny activation
+// operand and the scales are read through L2, one K-block ahead.
 //
 // The operand path is the prefill kernel's: FP8-E4M3 subnormal codes, one
 // v_mfma_f32_16x16x128_f8f6f4 per 16x16 block and K-block (two for 8-bit
@@ -94,45 +92,27 @@ __device__ __forceinline__ void load_scales(const GemmArgs& p, int gb, int n0, S
   s.sw = p.sw[(size_t)g * p.N + n0 + (lane & 15)];
 }
 
-// Weights of the batch starting at K-block gb for the wave's 16 rows n0..:
-// load j covers rows 4 j + lane / 16, bytes 16 * (lane % 16) of the row's
-// 256-byte run (K-block gb + (lane % 16) / 4, quarter lane % 4).  K-blocks
-// past the last one repeat it (in-row reads; never computed).
+// Weight fragments of the batch starting at K-block gb for the wave's panel
+// (rows n0 .. n0 + 15): load i is K-block gb + i, lane r + 16 q reading row
+// r's 16-byte chunk q.  K-blocks past the last one repeat it (never computed).
 __device__ __forceinline__ void load_w(const GemmArgs& p, int gb, int n0, u32x4 (&w)[4]) {
   const int lane = threadIdx.x & 63;
-  const int c = lane & 15;
-  const int g = min(gb + (c >> 2), p.K / kG - 1);
+  const int NG = p.K / kG;
+  const uint8_t* panel = p.W + (size_t)(n0 / 16) * NG * 1024 + (lane & 15) * 64 + (lane >> 4) * 16;
   #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = n0 + 4 * j + (lane >> 4);
-    const u32x4* src = reinterpret_cast<const u32x4*>(p.W + (size_t)row * (p.K / 2) +
-                                                      (size_t)g * 64 + (c & 3) * 16);
-    w[j] = __builtin_nontemporal_load(src);
-  }
-}
-
-// The wave's LDS buffer holds a batch as 16 rows x 256 bytes; row r's 16-byte
-// chunk c (K-block c / 4, quarter c % 4) sits at r * 256 + ((c ^ r) << 4).
-// Writes: 16 lanes fill one row's 256 bytes.  Fragment reads: 16 lanes read
-// 16 rows at one logical chunk, which the XOR spreads over all banks.
-__device__ __forceinline__ void store_w(uint8_t* buf, const u32x4 (&w)[4]) {
-  const int lane = threadIdx.x & 63;
-  const int c = lane & 15;
-  #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = 4 * j + (lane >> 4);
-    *reinterpret_cast<u32x4*>(buf + row * 256 + ((c ^ row) << 4)) = w[j];
+  for (int i = 0; i < 4; ++i) {
+    const int g = min(gb + i, NG - 1);
+    w[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(panel + (size_t)g * 1024));
   }
 }
 
 template <int R, bool DIAG>
-__device__ __forceinline__ void compute_step(const GemmArgs& p, const uint8_t* wbuf, int i,
-                                             int g, bool b8, int n0, const AStep<R>& s,
+__device__ __forceinline__ void compute_step(const GemmArgs& p, const u32x4& wraw, int i, int g,
+                                             bool b8, int n0, const AStep<R>& s,
                                              const SBatch<R>& sc, f32x4 (&C)[R]) {
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, q4 = lane >> 4;
   const int NG = p.K / kG;
-  const u32x4 wraw = *reinterpret_cast<const u32x4*>(wbuf + r16 * 256 + (((4 * i + q4) ^ r16) << 4));
   u32x4 wlo, whi;
   unpack4(wraw, wlo, whi);
   const i32x8 wf = {(int)wlo[0], (int)wlo[1], (int)wlo[2], (int)wlo[3],
@@ -198,14 +178,13 @@ __device__ __forceinline__ void issue_point() {
 // of K-block gb is in `x` on entry; `x` and `y` alternate, and the step of
 // K-block gb + 4 is in `x` on exit.
 template <int R, bool DIAG>
-__device__ __forceinline__ void batch(const GemmArgs& p, uint8_t* wbuf, int gb, int g1, int n0,
-                                      int col, int& aoff, const u32x4 (&wc)[4], u32x4 (&wn)[4],
+__device__ __forceinline__ void batch(const GemmArgs& p, int gb, int g1, int n0, int col,
+                                      int& aoff, const u32x4 (&wc)[4], u32x4 (&wn)[4],
                                       const SBatch<R>& sc, SBatch<R>& sn, AStep<R>& x,
                                       AStep<R>& y, f32x4 (&C)[R]) {
   const int NG = p.K / kG;
   load_w(p, gb + kD, n0, wn);
   load_scales<R>(p, gb + kD, n0, sn);
-  store_w(wbuf, wc);
   #pragma unroll
   for (int i = 0; i < kD; ++i) {
     const int g = gb + i;
@@ -217,7 +196,7 @@ __device__ __forceinline__ void batch(const GemmArgs& p, uint8_t* wbuf, int gb, 
     AStep<R>& nxt = (i & 1) ? x : y;
     load_a<R>(p, gn, an, col, nxt);
     issue_point();
-    if (g < g1) compute_step<R, DIAG>(p, wbuf, i, g, b8, n0, cur, sc, C);
+    if (g < g1) compute_step<R, DIAG>(p, wc[i], i, g, b8, n0, cur, sc, C);
     aoff = an;
   }
 }
@@ -230,7 +209,6 @@ __device__ __forceinline__ void batch(const GemmArgs& p, uint8_t* wbuf, int gb, 
 // L2: measured ~12x slower for a 70B-sized weight stream.)
 template <int R, bool DIAG>
 __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
-  __shared__ __attribute__((aligned(16))) uint8_t wlds[kWaves][16 * 256];
   __shared__ f32x4 red[kWaves][R][64];
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, q4 = lane >> 4;
@@ -249,7 +227,6 @@ __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
   #pragma unroll
   for (int r = 0; r < R; ++r) C[r] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (active && g0 < g1) {
-    uint8_t* wbuf = wlds[wave];
     u32x4 wa[4], wb[4];
     SBatch<R> sa_, sb_;
     AStep<R> x, y;
@@ -258,10 +235,10 @@ __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
     load_scales<R>(p, g0, n0, sa_);
     load_a<R>(p, g0, aoff, col, x);
     for (int gb = g0;;) {
-      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wa, wb, sa_, sb_, x, y, C);
+      batch<R, DIAG>(p, gb, g1, n0, col, aoff, wa, wb, sa_, sb_, x, y, C);
       gb += kD;
       if (gb >= g1) break;
-      batch<R, DIAG>(p, wbuf, gb, g1, n0, col, aoff, wb, wa, sb_, sa_, x, y, C);
+      batch<R, DIAG>(p, gb, g1, n0, col, aoff, wb, wa, sb_, sa_, x, y, C);
       gb += kD;
       if (gb >= g1) break;
     }

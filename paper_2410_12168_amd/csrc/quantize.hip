@@ -213,8 +213,9 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(const uint16_t* __res
   }
 }
 
-// Weights: pair p -> (row n = p / NG, block g = p % NG); consecutive pairs are
-// consecutive blocks of one row, contiguous in the row-major W_packed.
+// Weights: pair p -> (row n = p / NG, block g = p % NG).  W_packed is stored
+// in 16-row panels: row n's block g at ((n / 16 * NG + g) * 16 + n % 16) * 64,
+// so every GEMM reads a panel's K-block as one contiguous kilobyte.
 template <bool kPerm>
 __global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t* __restrict__ W,
                                                       const int32_t* __restrict__ perm,
@@ -242,7 +243,8 @@ __global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t* __restrict
   Codes c;
   uint16_t s16 = quantize8(x, a, 7.0f, c);
   if (!valid) return;
-  *reinterpret_cast<uint32_t*>(Wp + (size_t)n * (K / 2) + (size_t)g * 64 + 4 * lane16) = pack4(c);
+  const size_t chunk = ((size_t)(n / 16) * NG + g) * 16 + (size_t)(n % 16);
+  *reinterpret_cast<uint32_t*>(Wp + chunk * 64 + 4 * lane16) = pack4(c);
   if (lane16 == 0) sw[(size_t)g * N + n] = s16;
 }
 

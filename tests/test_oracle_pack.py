@@ -8,6 +8,7 @@ float8_e4m3fn conversion (an independent library routine), not by re-typing
 the oracle's bit layout.
 """
 import numpy as np
+import pytest
 import torch
 
 import oracle
@@ -82,13 +83,28 @@ def test_pack_act_block_major_layout():
         off += M * B
 
 
-def test_pack_weight_row_major_layout():
-    N, K, G = 4, 384, 128
+def test_pack_weight_panel_layout():
+    # 16-row panels: row n, block g at ((n // 16 * NG + g) * 16 + n % 16) * 64
+    N, K, G = 48, 384, 128
+    NG = K // G
     rng = np.random.default_rng(6)
     qw = rng.integers(-7, 8, (N, K)).astype(np.int8)
-    buf = oracle.pack_weight(qw, G)
-    assert buf.shape == (N, K // 2)
+    flat = oracle.pack_weight(qw, G).reshape(-1)
+    assert flat.size == N * K // 2
+    seen = np.zeros(flat.size, bool)
     for n in range(N):
-        for g in range(K // G):
-            dec = decode4(buf[n, g * 64:(g + 1) * 64].copy())
+        for g in range(NG):
+            off = ((n // 16 * NG + g) * 16 + n % 16) * 64
+            dec = decode4(flat[off:off + 64].copy())
             assert np.array_equal(dec, qw[n, g * G:(g + 1) * G].astype(np.float32))
+            seen[off:off + 64] = True
+    assert seen.all()  # every byte belongs to exactly one (row, block)
+    # one panel's block is one contiguous run of 16 rows
+    run = flat[(1 * NG + 2) * 1024:(1 * NG + 2) * 1024 + 1024].reshape(16, 64)
+    for r in range(16):
+        assert np.array_equal(decode4(run[r].copy()), qw[16 + r, 2 * G:3 * G].astype(np.float32))
+
+
+def test_pack_weight_rejects_partial_panel():
+    with pytest.raises(ValueError):
+        oracle.pack_weight(np.zeros((24, 256), np.int8), 128)
