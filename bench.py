@@ -104,6 +104,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--m", type=int, default=0, help="tokens (default: the workload's)")
     ap.add_argument("--frac8", type=float, default=1 / 16)
+    ap.add_argument("--placement", default="contiguous", choices=["contiguous", "random"],
+                    help="where the 8-bit blocks sit (a contiguous run, or a seeded random subset)")
     ap.add_argument("--layers", default="",
                     help="comma-separated subset of the workload's layers (default: all)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -161,7 +163,7 @@ def main():
             n8 = int((prec == 8).sum())
         else:
             n8 = int(round(NG * args.frac8))
-            prec = synth.prec_map(NG, n8)
+            prec = synth.prec_map(NG, n8, args.placement, seed=args.seed)
             X16 = synth.activations(args.seed, M, K, prec)
             X = torch.from_numpy(X16.view(np.int16)).to(dev).view(torch.float16)
         Wp, sw = comet.pack_w4(Wd, perm=perm)
@@ -289,11 +291,11 @@ def main():
                          f"tokens, G=128, " +
                          (f"calibrated channel permutation ({', '.join(str(L['n8']) for L in layers)}"
                           f" 8-bit blocks)" if args.perm else
-                          f"{args.frac8:.4g} of activation blocks 8-bit")),
+                          f"{args.frac8:.4g} of activation blocks 8-bit ({args.placement})")),
             "M": M, "G": 128, "frac8": (round(float(np.mean([L['n8'] / (L['K'] // 128)
                                                           for L in layers])), 4)
                                         if args.perm else args.frac8),
-            "perm": bool(args.perm), "seed": args.seed,
+            "perm": bool(args.perm), "placement": args.placement, "seed": args.seed,
             "operands": "int4 weights, int4/int8 activation codes on FP8-E4M3 MFMA, fp32 dequant",
         },
         "roofline": roof,
