@@ -50,6 +50,10 @@ def _load():
         "orc_plan_channel_perm": (I, [P, I, I, ctypes.c_float, ctypes.c_float, P, P, P]),
         "orc_kv4_quantize": (I, [P, I, I, I, P, P]),
         "orc_kv4_dequantize": (I, [P, P, I, I, I, P]),
+        "orc_exp_f32": (ctypes.c_float, [ctypes.c_float]),
+        "orc_silu_f32": (ctypes.c_float, [ctypes.c_float]),
+        "orc_swiglu_f16": (ctypes.c_uint16, [ctypes.c_uint16, ctypes.c_uint16]),
+        "orc_swiglu_quantize": (I, [P, I, I, I, P, P, P, I]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -264,3 +268,37 @@ def kv4_dequantize(codes, params, G: int = 128) -> np.ndarray:
     if _load().orc_kv4_dequantize(_p(codes), _p(params), T, C, G, _p(out)):
         raise ValueError("bad arguments to kv4_dequantize")
     return out
+
+
+# --- SwiGLU and next-layer quantization ----------------------------------------------
+
+def exp_f32(x) -> np.ndarray:
+    x = np.asarray(x, np.float32).reshape(-1)
+    f = _load().orc_exp_f32
+    return np.array([f(float(v)) for v in x], np.float32)
+
+
+def silu_f32(x) -> np.ndarray:
+    x = np.asarray(x, np.float32).reshape(-1)
+    f = _load().orc_silu_f32
+    return np.array([f(float(v)) for v in x], np.float32)
+
+
+def swiglu_f16(g16, u16) -> np.ndarray:
+    g16 = np.asarray(g16, np.uint16).reshape(-1)
+    u16 = np.asarray(u16, np.uint16).reshape(-1)
+    f = _load().orc_swiglu_f16
+    return np.array([f(int(a), int(b)) for a, b in zip(g16, u16)], np.uint16)
+
+
+def swiglu_quantize(gu16, prec, G: int = 128, nthreads: int = 0):
+    """gu16 uint16 [M][2I] (2G-wide gate/up column groups) -> (A_packed, sa16 [I/G][M])."""
+    gu16 = _c(gu16, np.uint16)
+    prec = _c(prec, np.uint8)
+    M, N = gu16.shape
+    I = N // 2
+    A = np.empty(act_packed_bytes(prec, M, I, G), np.uint8)
+    sa = np.empty((I // G, M), np.uint16)
+    if _load().orc_swiglu_quantize(_p(gu16), M, I, G, _p(prec), _p(A), _p(sa), nthreads):
+        raise ValueError("oracle rejected the swiglu inputs")
+    return A, sa

@@ -445,3 +445,66 @@ int orc_kv4_dequantize(const uint8_t* codes, const uint16_t* params, int T, int 
     }
   return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* SwiGLU and the next layer's quantization (the step after the path: the    */
+/* gate/up GEMM's output becomes the down projection's input, h = SiLU(gate) */
+/* * up, quantized by FMPQ in 128-channel blocks, Sec. 3.2).                 */
+/*                                                                           */
+/* exp is written out so that a GPU kernel can follow the same fp32 steps:   */
+/* Cody-Waite reduction x = k ln2 + r with k = rint(x log2 e) and ln2 split  */
+/* into a 24-bit-exact high part and a low part, exp(r) by its Taylor series */
+/* to degree 7 in Horner form, then the exact scaling by 2^k.  The input is  */
+/* clamped to [-87, 88], which keeps k within the normal exponent range.     */
+/* ------------------------------------------------------------------------- */
+
+float orc_exp_f32(float x) {
+  if (x > 88.0f) x = 88.0f;
+  if (x < -87.0f) x = -87.0f;
+  const float log2e = 1.44269504088896341f;
+  const float ln2_hi = 0.693145751953125f;     /* 0x3F317200: 16 significant bits */
+  const float ln2_lo = 1.42860682030941723e-6f; /* ln 2 - ln2_hi */
+  const float k = rintf(x * log2e);
+  float r = fmaf(-k, ln2_hi, x);
+  r = fmaf(-k, ln2_lo, r);
+  /* 1/n! for n = 7 .. 0 */
+  const float c[8] = {1.98412698412698413e-4f, 1.38888888888888889e-3f,
+                      8.33333333333333333e-3f, 4.16666666666666667e-2f,
+                      1.66666666666666667e-1f, 0.5f, 1.0f, 1.0f};
+  float p = c[0];
+  for (int i = 1; i < 8; ++i) p = fmaf(p, r, c[i]);
+  return ldexpf(p, (int)k);
+}
+
+float orc_silu_f32(float x) { return x * (1.0f / (1.0f + orc_exp_f32(-x))); }
+
+/* h = fp16(SiLU(g) * u) for fp16 g, u. */
+uint16_t orc_swiglu_f16(uint16_t g, uint16_t u) {
+  return orc_f16_from_f32(orc_silu_f32(orc_f32_from_f16(g)) * orc_f32_from_f16(u));
+}
+
+int orc_swiglu_quantize(const uint16_t* gu, int M, int I, int G, const uint8_t* prec,
+                        uint8_t* A_packed, uint16_t* sa16, int nthreads) {
+  if (M < 0 || I <= 0 || G <= 0 || I % G || G > 1024) return -1;
+  uint16_t* h = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)M * (size_t)I);
+  int8_t* q = (int8_t*)malloc((size_t)M * (size_t)I);
+  if (!h || !q) {
+    free(h);
+    free(q);
+    return -1;
+  }
+  /* gate/up columns come in 2G-wide groups: gate of channels jG..jG+G-1, then
+   * up of the same channels */
+  for (int m = 0; m < M; ++m)
+    for (int c = 0; c < I; ++c) {
+      const int j = c / G, i = c % G;
+      const uint16_t g = gu[(size_t)m * 2 * I + (size_t)j * 2 * G + i];
+      const uint16_t u = gu[(size_t)m * 2 * I + (size_t)j * 2 * G + G + i];
+      h[(size_t)m * I + c] = orc_swiglu_f16(g, u);
+    }
+  int rc = orc_quantize_act(h, prec, M, I, G, q, sa16, nthreads);
+  if (!rc) rc = orc_pack_act(q, prec, M, I, G, A_packed);
+  free(h);
+  free(q);
+  return rc;
+}

@@ -121,6 +121,22 @@ int orc_kv4_quantize(const uint16_t* X, int T, int C, int G, uint8_t* codes, uin
 int orc_kv4_dequantize(const uint8_t* codes, const uint16_t* params, int T, int C, int G,
                        uint16_t* out);
 
+/* SwiGLU and next-layer quantization (the step after the W4Ax GEMM).
+ * orc_exp_f32: exp by Cody-Waite reduction (k = rint(x log2e), r = x - k ln2
+ *   with ln2 split in two, fmas), Taylor series to degree 7 in Horner form
+ *   (fmas), ldexp by k; input clamped to [-87, 88].
+ * orc_silu_f32(x) = x * (1 / (1 + orc_exp_f32(-x))), each an fp32 operation.
+ * orc_swiglu_f16(g, u) = fp16(orc_silu_f32(g) * u).
+ * orc_swiglu_quantize: gu fp16 [M][2I] whose columns come in 2G-wide groups
+ *   (gate of channels jG .. jG+G-1, then up of the same channels); h [M][I] =
+ *   swiglu(gate, up), then FMPQ quantization and packing of h with map prec
+ *   [I/G] into A_packed / sa16 [I/G][M] (as orc_quantize_act + orc_pack_act). */
+float orc_exp_f32(float x);
+float orc_silu_f32(float x);
+uint16_t orc_swiglu_f16(uint16_t g, uint16_t u);
+int orc_swiglu_quantize(const uint16_t* gu, int M, int I, int G, const uint8_t* prec,
+                        uint8_t* A_packed, uint16_t* sa16, int nthreads);
+
 #ifdef __cplusplus
 }
 #endif
