@@ -42,6 +42,9 @@ WORKLOADS = {
     "llama3-8b-prefill": dict(M=2048, layers="LLAMA3_8B"),
     # few-token regime: the gate_up layer streams its 4-bit weights from HBM
     "llama3-70b-decode": dict(M=8, layers="LLAMA3_70B", only="gate_up", rotate=6),
+    # LLaMA-3-70B MLP: quantize x, gate/up GEMM with SwiGLU and the down
+    # projection's quantization fused into its epilogue, down GEMM
+    "llama3-70b-mlp": dict(M=4096, mlp=True),
     # KV4 cache quantization of a prefill batch (8 prompts x 4096 tokens): the
     # K and V rows of every layer (8 KV heads x head_dim 128 = 1024 channels,
     # groups of 128)
@@ -111,6 +114,9 @@ def parse():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one device-to-device copy of this many MiB (a "
                          "known-size reference for HBM byte counters)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="llama3-70b-mlp: gate/up GEMM to fp16, then a separate SwiGLU-quantize "
+                         "kernel (instead of the fused epilogue)")
     ap.add_argument("--perm", action="store_true",
                     help="calibrated channel permutation: activations with scattered outlier "
                          "channels, map and permutation planned from sampled maxima, permuted "
@@ -137,6 +143,8 @@ def main():
     wl = WORKLOADS[args.workload]
     if "T" in wl:
         return bench_kv4(args, wl, dev)
+    if wl.get("mlp"):
+        return bench_mlp(args, wl, dev)
     M = args.m or wl["M"]
     shapes = getattr(synth, wl["layers"])
     if "only" in wl:
@@ -353,6 +361,95 @@ def cpu_baseline(layers, rows_per_layer: int) -> dict:
                             for L in layers) + " (quantize + fp64-dequant GEMM)",
         "parity_max_rel": worst, "parity_norm_rel": worst_norm, "parity_ok": worst <= 2e-3,
     }
+
+
+def bench_mlp(args, wl, dev):
+    """One LLaMA-3-70B MLP over M tokens: quantize x (K = 8192), gate/up W4Ax
+    GEMM (N = 2 x 28672, gate/up rows in 256-wide groups) whose epilogue forms
+    h = SiLU(gate) * up and quantizes it for the down projection, then the
+    down W4Ax GEMM (28672 -> 8192).  --unfused writes the gate/up output in
+    fp16 and runs the SwiGLU quantizer as its own kernel instead."""
+    import torch
+
+    import paper_2410_12168_amd as comet
+    import synth
+
+    M = args.m or wl["M"]
+    (K1, N1), (K2, N2) = synth.LLAMA3_70B["gate_up"], synth.LLAMA3_70B["down"]
+    I = N1 // 2
+    t_setup = time.time()
+    NG1, NG2 = K1 // 128, K2 // 128
+    prec1 = synth.prec_map(NG1, int(round(NG1 * args.frac8)), args.placement, seed=args.seed)
+    prec2 = synth.prec_map(NG2, int(round(NG2 * args.frac8)), args.placement, seed=args.seed + 1)
+    X16 = synth.activations(args.seed, M, K1, prec1)
+    X = torch.from_numpy(X16.view(np.int16)).to(dev).view(torch.float16)
+    packed = []
+    for tid_seed, (N, K) in ((args.seed, (N1, K1)), (args.seed + 1, (N2, K2))):
+        Wd = torch.from_numpy(synth.weights(tid_seed, N, K).view(np.int16)).to(dev).view(torch.float16)
+        packed.append(comet.pack_w4(Wd))
+        del Wd
+    (Wp1, sw1), (Wp2, sw2) = packed
+    A1 = torch.empty(comet.comet_act_packed_bytes(prec1, M, K1), dtype=torch.uint8, device=dev)
+    sa1 = torch.empty((NG1, M), dtype=torch.float16, device=dev)
+    A2 = torch.empty(comet.comet_act_packed_bytes(prec2, M, K2), dtype=torch.uint8, device=dev)
+    sa2 = torch.empty((NG2, M), dtype=torch.float16, device=dev)
+    gu = torch.empty((M, N1), dtype=torch.float16, device=dev) if args.unfused else None
+    y = torch.empty((M, N2), dtype=torch.float16, device=dev)
+    torch.cuda.synchronize()
+    t_setup = time.time() - t_setup
+
+    def step(ev=None):
+        comet.comet_fmpq_quantize_act(X, prec1, A1, sa1, M, K1)
+        if ev is not None:
+            ev[0].record()
+        if args.unfused:
+            comet.comet_w4ax_gemm(A1, prec1, sa1, Wp1, sw1, gu, M, N1, K1)
+            comet.comet_swiglu_quantize(gu, prec2, A2, sa2, M, I)
+        else:
+            comet.comet_w4ax_gemm_swiglu_quant(A1, prec1, sa1, Wp1, sw1, M, N1, K1, 128, prec2,
+                                               A2, sa2)
+        if ev is not None:
+            ev[1].record()
+        comet.comet_w4ax_gemm(A2, prec2, sa2, Wp2, sw2, y, M, N2, K2)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    gu_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    ops1, ops2 = 2.0 * M * N1 * K1, 2.0 * M * N2 * K2
+    value = (ops1 + ops2) / (ms_per_step * 1e-3) / 1e12
+    achieved = ops1 / (gu_ms * 1e-3) / 1e12
+    record = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp8",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: quantize x, gate/up W4Ax GEMM "
+                               f"{'then a separate SwiGLU-quantize kernel' if args.unfused else 'with SwiGLU + down-input quantization fused in its epilogue'}"
+                               f", down W4Ax GEMM, M={M} tokens, G=128, {args.frac8:.4g} of "
+                               f"activation blocks 8-bit",
+                   "M": M, "G": 128, "frac8": args.frac8, "fused": not args.unfused,
+                   "seed": args.seed},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_MFMA_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4),
+                     "traffic": None,
+                     "kernel": f"gate/up W4Ax GEMM{' + SwiGLU quantizer' if args.unfused else ' with fused SwiGLU epilogue'}"
+                               f" (M={M}, K={K1}, N={N1}): {gu_ms * 1e3:.2f} us per step"},
+        "setup_s": round(t_setup, 1),
+    }
+    print(json.dumps(record), flush=True)
 
 
 def bench_kv4(args, wl, dev):

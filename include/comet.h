@@ -188,6 +188,44 @@ COMET_API comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t*
                                const uint16_t* w_scales, uint16_t* out, int M, int N, int K,
                                int G, hipStream_t stream);
 
+/* SwiGLU and the next layer's quantization, fused into the W4Ax GEMM (the step
+ * after the path: in a LLaMA MLP the gate/up GEMM's output feeds the down
+ * projection through h = SiLU(gate) * up, whose activations FMPQ quantizes in
+ * 128-channel blocks, Sec. 3.2).  The GEMM is comet_w4ax_gemm's, but instead
+ * of storing its fp16 output the call writes the down projection's quantized
+ * input:
+ *   - the weight rows (output columns) come in 2G = 256-wide groups: rows
+ *     256 j .. 256 j + 127 are the gate rows and 256 j + 128 .. 256 j + 255
+ *     the up rows of channels 128 j .. 128 j + 127 (a caller interleaves W_gate
+ *     and W_up this way before comet_pack_w4); N = 2 I, a multiple of 256;
+ *   - with g, u the fp16-rounded GEMM outputs, h = fp16(SiLU(g) * u) where
+ *     SiLU(x) = x * (1 / (1 + exp(-x))) and exp follows fixed fp32 steps
+ *     (x clamped to [-87, 88]; k = rint(x log2 e); r = x - k ln2 by two fmas
+ *     with ln2 = 0.693145751953125 + 1.42860682030941723e-6; the Taylor series
+ *     of e^r to degree 7 in Horner form by fmas; ldexp(., k));
+ *   - h [M][I] is quantized with out_prec (host, I/G entries of 4 or 8) into
+ *     out_A_packed (device, comet_act_packed_bytes(out_prec, M, I, G) bytes)
+ *     and out_a_scales (device, fp16 [I/G][M]), exactly as
+ *     comet_fmpq_quantize_act would quantize h.
+ * A channel permutation for the down projection needs no runtime step here:
+ * permute the gate and up rows (and the down projection's weight columns,
+ * comet_pack_w4_perm) offline.  Other arguments and errors as comet_w4ax_gemm;
+ * M at most 2,097,120.  For M <= 48 the GEMM writes fp16 to a library-owned
+ * workspace (per device and stream) that comet_swiglu_quantize then reads. */
+COMET_API comet_status_t comet_w4ax_gemm_swiglu_quant(
+    const uint8_t* A_packed, const uint8_t* group_prec_map, const uint16_t* a_scales,
+    const uint8_t* W_packed, const uint16_t* w_scales, int M, int N, int K, int G,
+    const uint8_t* out_prec_map, uint8_t* out_A_packed, uint16_t* out_a_scales,
+    hipStream_t stream);
+
+/* The same SwiGLU and quantization on an fp16 gate/up output gu (device,
+ * [M][2I] with the 256-wide gate/up column groups above, 16-byte aligned),
+ * written to out_A_packed / out_a_scales as above.  I a multiple of G = 128;
+ * M at most 2,097,120. */
+COMET_API comet_status_t comet_swiglu_quantize(const uint16_t* gu, const uint8_t* out_prec_map,
+                                               uint8_t* out_A_packed, uint16_t* out_a_scales,
+                                               int M, int I, int G, hipStream_t stream);
+
 /* Diagnostic form of the same contraction: writes the exact per-block integer
  * sums acc[m - m0][n - n0][g] = sum_{c<G} qa[m][gG+c] * qw[n][gG+c] (int32)
  * for the window m0 <= m < m1, n0 <= n < n1, computed by the GEMM's own

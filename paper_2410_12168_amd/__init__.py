@@ -60,6 +60,8 @@ def lib():
         "comet_plan_channel_perm": (I, [P, I, I, ctypes.c_float, ctypes.c_float, P, P, P]),
         "comet_kv4_quantize": (I, [P, P, P, I, I, I, P]),
         "comet_kv4_dequantize": (I, [P, P, P, I, I, I, P]),
+        "comet_w4ax_gemm_swiglu_quant": (I, [P, P, P, P, P, I, I, I, I, P, P, P, P]),
+        "comet_swiglu_quantize": (I, [P, P, P, P, I, I, I, P]),
         "comet_status_str": (ctypes.c_char_p, [I]),
         "comet_last_error": (ctypes.c_char_p, []),
         "comet_release_caches": (None, []),
@@ -153,6 +155,24 @@ def comet_kv4_quantize(X, codes, params, T: int, C: int, G: int = 128, stream=No
 def comet_kv4_dequantize(codes, params, out, T: int, C: int, G: int = 128, stream=None) -> None:
     _check(lib().comet_kv4_dequantize(_ptr(codes), _ptr(params), _ptr(out), T, C, G,
                                       _stream(stream)))
+
+
+def comet_w4ax_gemm_swiglu_quant(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int,
+                                 N: int, K: int, G: int, out_prec_map, out_A_packed, out_a_scales,
+                                 stream=None) -> None:
+    m = _map(group_prec_map)
+    om = _map(out_prec_map)
+    _check(lib().comet_w4ax_gemm_swiglu_quant(_ptr(A_packed), _ptr(m), _ptr(a_scales),
+                                              _ptr(W_packed), _ptr(w_scales), M, N, K, G,
+                                              _ptr(om), _ptr(out_A_packed), _ptr(out_a_scales),
+                                              _stream(stream)))
+
+
+def comet_swiglu_quantize(gu, out_prec_map, out_A_packed, out_a_scales, M: int, I: int,
+                          G: int = G, stream=None) -> None:
+    om = _map(out_prec_map)
+    _check(lib().comet_swiglu_quantize(_ptr(gu), _ptr(om), _ptr(out_A_packed),
+                                       _ptr(out_a_scales), M, I, G, _stream(stream)))
 
 
 def comet_w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, out, M: int, N: int,
@@ -282,6 +302,38 @@ def w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int, N:
     comet_w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, out, M, N, K, G,
                     stream)
     return out
+
+
+def w4ax_gemm_swiglu_quant(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int, N: int,
+                           K: int, out_prec_map, stream=None):
+    """Fused gate/up GEMM + SwiGLU + quantization for the next layer.
+    Returns (out_A_packed uint8, out_a_scales float16 [I/G][M]), I = N / 2."""
+    import torch
+
+    I = N // 2
+    nbytes = comet_act_packed_bytes(out_prec_map, M, I)
+    if nbytes == 0:
+        raise CometError(1, "invalid output map or shape")
+    A2 = torch.empty(nbytes, dtype=torch.uint8, device=A_packed.device)
+    sa2 = torch.empty((I // G, M), dtype=torch.float16, device=A_packed.device)
+    comet_w4ax_gemm_swiglu_quant(A_packed, group_prec_map, a_scales, W_packed, w_scales, M, N, K,
+                                 G, out_prec_map, A2, sa2, stream)
+    return A2, sa2
+
+
+def swiglu_quantize(gu, out_prec_map, stream=None):
+    """gu: float16 [M][2I] CUDA tensor (256-wide gate/up groups) -> (A_packed, a_scales)."""
+    import torch
+
+    M, N = gu.shape
+    I = N // 2
+    nbytes = comet_act_packed_bytes(out_prec_map, M, I)
+    if nbytes == 0:
+        raise CometError(1, "invalid output map or shape")
+    A2 = torch.empty(nbytes, dtype=torch.uint8, device=gu.device)
+    sa2 = torch.empty((I // G, M), dtype=torch.float16, device=gu.device)
+    comet_swiglu_quantize(gu, out_prec_map, A2, sa2, M, I, G, stream)
+    return A2, sa2
 
 
 def w4ax_gemm_acc(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int, N: int, K: int,

@@ -143,6 +143,8 @@ struct Workspace {
   size_t partial_floats = 0;
   int* counters = nullptr;
   size_t ncounters = 0;
+  uint16_t* tmp = nullptr;  // fp16 gate/up output of the few-token SwiGLU path
+  size_t tmp_bytes = 0;
 };
 
 std::map<PlanKey, DevicePlan> g_plans;
@@ -265,10 +267,44 @@ comet_status_t get_workspace(int dev, hipStream_t stream, size_t partial_floats,
   return COMET_OK;
 }
 
+// fp16 buffer of the few-token SwiGLU path on (device, stream), grown on
+// demand.  Caller holds g_mu.
+comet_status_t get_tmp(int dev, hipStream_t stream, size_t bytes, uint16_t** out) {
+  Workspace& ws = g_ws[{dev, stream}];
+  if (bytes > ws.tmp_bytes) {
+    if (ws.tmp) {
+      hipError_t e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) return fail(COMET_ERR_HIP, "workspace sync: %s", hipGetErrorString(e));
+      (void)hipFree(ws.tmp);
+      ws.tmp = nullptr;
+      ws.tmp_bytes = 0;
+    }
+    if (std::getenv("COMET_TEST_FAIL_ALLOC")) return fail(COMET_ERR_OOM, "workspace allocation failed (forced)");
+    hipError_t e = hipMalloc(&ws.tmp, bytes);
+    if (e != hipSuccess) {
+      ws.tmp = nullptr;
+      return fail(COMET_ERR_OOM, "workspace allocation: %s", hipGetErrorString(e));
+    }
+    ws.tmp_bytes = bytes;
+  }
+  *out = ws.tmp;
+  return COMET_OK;
+}
+
+// The GEMM.  With `swiglu` (non-null) the output is not stored: the tile
+// kernels' epilogue quantizes h = SiLU(gate) * up straight into swiglu->A /
+// swiglu->sa; the few-token kernel writes fp16 to a workspace that the SwiGLU
+// quantizer then reads.
+struct SwigluOut {
+  uint8_t* A;
+  uint16_t* sa;
+  comet::BlockMap map;
+};
+
 comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* sa,
                         const uint8_t* W, const uint16_t* sw, uint16_t* out, int32_t* acc, int M,
                         int N, int K, const comet::BlockMap& map, int m0, int m1, int n0, int n1,
-                        hipStream_t stream) {
+                        hipStream_t stream, const SwigluOut* swiglu = nullptr) {
   int dev;
   DeviceInfo info;
   comet_status_t st = current_device(&dev, &info);
@@ -318,8 +354,23 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   a.win_n0 = n0;
   a.win_n1 = n1;
   a.map = map;
+  if (swiglu && skinny) {
+    uint16_t* tmp;
+    if ((st = get_tmp(dev, stream, (size_t)M * N * sizeof(uint16_t), &tmp))) return st;
+    a.out = tmp;
+    if ((st = launched(comet::launch_gemm_skinny(a, false, stream), "gemm launch"))) return st;
+    return launched(comet::launch_swiglu_quantize(tmp, swiglu->A, swiglu->sa, M, N / 2,
+                                                  swiglu->map, stream),
+                    "swiglu_quantize launch");
+  }
+  if (swiglu) {
+    a.out_A = swiglu->A;
+    a.out_sa = swiglu->sa;
+    a.out_map = swiglu->map;
+  }
   if (skinny) return launched(comet::launch_gemm_skinny(a, diag, stream), "gemm launch");
-  return launched(comet::launch_gemm(a, plan->host.num_wgs, diag, plan->host.tile_m, stream),
+  return launched(comet::launch_gemm(a, plan->host.num_wgs, diag, swiglu != nullptr,
+                                     plan->host.tile_m, stream),
                   "gemm launch");
 }
 
@@ -473,6 +524,50 @@ comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* prec,
                   0, 0, stream);
 }
 
+comet_status_t comet_w4ax_gemm_swiglu_quant(const uint8_t* A_packed, const uint8_t* prec,
+                                            const uint16_t* a_scales, const uint8_t* W_packed,
+                                            const uint16_t* w_scales, int M, int N, int K, int G,
+                                            const uint8_t* out_prec, uint8_t* out_A_packed,
+                                            uint16_t* out_a_scales, hipStream_t stream) {
+  if (!out_A_packed || !out_a_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (N < 256 || N % 256)
+    return fail(COMET_ERR_INVALID_ARG, "N=%d must be a positive multiple of 256 (2G-wide gate/up "
+                "column groups)", N);
+  if (!aligned16(out_A_packed) || !aligned16(out_a_scales))
+    return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  comet::BlockMap map;
+  // `out` is not written on this path; a non-null placeholder passes the common checks
+  comet_status_t st = gemm_common(A_packed, prec, a_scales, W_packed, w_scales, out_A_packed, M,
+                                  N, K, G, &map);
+  if (st) return st;
+  if (M > kMaxQuantRows)
+    return fail(COMET_ERR_UNSUPPORTED, "M=%d exceeds %d rows per call", M, kMaxQuantRows);
+  SwigluOut so{out_A_packed, out_a_scales, {}};
+  if ((st = make_map(out_prec, N / 2 / G, &so.map))) return st;
+  return run_gemm(A_packed, prec, a_scales, W_packed, w_scales, nullptr, nullptr, M, N, K, map, 0,
+                  0, 0, 0, stream, &so);
+}
+
+comet_status_t comet_swiglu_quantize(const uint16_t* GU, const uint8_t* out_prec,
+                                     uint8_t* out_A_packed, uint16_t* out_a_scales, int M, int I,
+                                     int G, hipStream_t stream) {
+  if (!GU || !out_A_packed || !out_a_scales) return fail(COMET_ERR_INVALID_ARG, "null pointer");
+  if (M < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d must be >= 1", M);
+  if (M > kMaxQuantRows)
+    return fail(COMET_ERR_UNSUPPORTED, "M=%d exceeds %d rows per call", M, kMaxQuantRows);
+  comet_status_t st = check_kg(I, G);
+  if (st) return st;
+  if (!aligned16(GU) || !aligned16(out_A_packed) || !aligned16(out_a_scales))
+    return fail(COMET_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  comet::BlockMap map;
+  if ((st = make_map(out_prec, I / G, &map))) return st;
+  int dev;
+  DeviceInfo info;
+  if ((st = current_device(&dev, &info))) return st;
+  return launched(comet::launch_swiglu_quantize(GU, out_A_packed, out_a_scales, M, I, map, stream),
+                  "swiglu_quantize launch");
+}
+
 comet_status_t comet_w4ax_gemm_acc(const uint8_t* A_packed, const uint8_t* prec,
                                    const uint16_t* a_scales, const uint8_t* W_packed,
                                    const uint16_t* w_scales, int32_t* acc, int M, int N, int K,
@@ -543,6 +638,7 @@ void comet_release_caches(void) {
     (void)hipSetDevice(kv.first.first);
     (void)hipFree(kv.second.partials);
     (void)hipFree(kv.second.counters);
+    (void)hipFree(kv.second.tmp);
   }
   if (cur >= 0) (void)hipSetDevice(cur);
   g_plans.clear();

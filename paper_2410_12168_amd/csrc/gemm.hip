@@ -37,8 +37,10 @@
 #include <hip/hip_fp16.h>
 #include <stdint.h>
 
+#include "fmpq.h"
 #include "kernels.h"
 #include "operand.h"
+#include "swiglu.h"
 
 namespace comet {
 
@@ -62,6 +64,7 @@ struct Geo {
   static constexpr int Buf = A + S;                // one activation stage, double-buffered
   static constexpr int Lds = 2 * Buf + 3 * kWr;
   static_assert(TM == 256 || TM == 128, "tile heights");
+  static_assert(TM * 136 * 2 <= Lds, "SwiGLU epilogue buffer fits in LDS");
 };
 
 // LDS layout of one activation stage: A (TM rows x 128 B), then the
@@ -396,9 +399,73 @@ __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o, u
 // Epilogue of a work unit: a whole tile is stored as fp16; a split tile
 // publishes this slot's fp32 partial, and the last workgroup to arrive adds
 // the partials in slot order and stores fp16.
+// SwiGLU epilogue (the step after the path, fused): the tile's columns 0-127
+// are the gate and 128-255 the up outputs of channels 128 j .. 128 j + 127
+// (j = n0 / 256).  The up waves put fp16(up) into LDS, the gate waves turn
+// each entry into h = SiLU(fp16(gate)) * up (fp16), and then 16 lanes per row
+// quantize the row's 128 channels of h as the activation quantizer does,
+// into block j of the next layer's A_packed.  `lds` is free by now.
 template <int TM>
+__device__ __forceinline__ void swiglu_tile(const GemmArgs& p, int m0, int n0,
+                                            f32x4 (&C)[Geo<TM>::RB][kCB], uint8_t* lds) {
+  constexpr int kRB = Geo<TM>::RB;
+  constexpr int kHP = 136;  // row pitch in halves: 128 channels + 16 bytes
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const int wr = (wave >> 2) * Geo<TM>::WM, wq = wave & 3;
+  uint16_t* H = reinterpret_cast<uint16_t*>(lds);
+  __syncthreads();
+  if (wq >= 2) {
+    #pragma unroll
+    for (int rb = 0; rb < kRB; ++rb)
+      #pragma unroll
+      for (int cb = 0; cb < kCB; ++cb)
+        #pragma unroll
+        for (int i = 0; i < 4; ++i)
+          H[(wr + rb * 16 + 4 * q4 + i) * kHP + (wq - 2) * 64 + cb * 16 + r16] =
+              __half_as_ushort(__float2half_rn(C[rb][cb][i]));
+  }
+  __syncthreads();
+  if (wq < 2) {
+    #pragma unroll
+    for (int rb = 0; rb < kRB; ++rb)
+      #pragma unroll
+      for (int cb = 0; cb < kCB; ++cb)
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          uint16_t* h = H + (wr + rb * 16 + 4 * q4 + i) * kHP + wq * 64 + cb * 16 + r16;
+          *h = swiglu_f16(__half_as_ushort(__float2half_rn(C[rb][cb][i])), *h);
+        }
+  }
+  __syncthreads();
+  const int j = n0 / kTileN;
+  const bool b8 = (p.out_map.bits[j >> 6] >> (j & 63)) & 1;
+  const size_t base = (size_t)p.M * 64 * (size_t)(j + n8_before(p.out_map, j));
+  const int lane16 = threadIdx.x & 15;
+  for (int r = threadIdx.x >> 4; r < TM; r += kThreads / 16) {
+    float x[8];
+    load8(H + r * kHP + 8 * lane16, x);
+    float a = 0.0f;
+    #pragma unroll
+    for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
+    a = max16(a);
+    Codes c;
+    const uint16_t s16 = quantize8(x, a, b8 ? 127.0f : 7.0f, c);
+    const int m = m0 + r;
+    if (m >= p.M) continue;
+    if (b8)
+      *reinterpret_cast<uint2*>(p.out_A + base + (size_t)m * 128 + 8 * lane16) = pack8(c);
+    else
+      *reinterpret_cast<uint32_t*>(p.out_A + base + (size_t)m * 64 + 4 * lane16) = pack4(c);
+    if (lane16 == 0) p.out_sa[(size_t)j * p.M + m] = s16;
+  }
+}
+
+template <int TM, bool SWIGLU>
 __device__ __forceinline__ void store_tile(const GemmArgs& p, const WorkUnit& unit, int m0, int n0,
-                                           f32x4 (&C)[Geo<TM>::RB][kCB], int* s_last) {
+                                           f32x4 (&C)[Geo<TM>::RB][kCB], int* s_last,
+                                           uint8_t* lds) {
   constexpr int kRB = Geo<TM>::RB;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -444,6 +511,10 @@ __device__ __forceinline__ void store_tile(const GemmArgs& p, const WorkUnit& un
     }
     if (threadIdx.x == 0) p.counters[base] = 0;  // ready for the next launch
   }
+  if constexpr (SWIGLU) {
+    swiglu_tile<TM>(p, m0, n0, C, lds);
+    return;
+  }
   #pragma unroll
   for (int rb = 0; rb < kRB; ++rb)
     #pragma unroll
@@ -458,7 +529,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& p, const WorkUnit& un
     }
 }
 
-template <int TM, bool DIAG>
+template <int TM, bool DIAG, bool SWIGLU>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
   constexpr int kRB = Geo<TM>::RB, kBuf = Geo<TM>::Buf;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -499,13 +570,13 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
                           n0, st, C);
     if (DIAG) continue;
 
-    store_tile<TM>(p, unit, m0, n0, C, &s_last);
+    store_tile<TM, SWIGLU>(p, unit, m0, n0, C, &s_last, smem);
   }
 }
 
 
 // ---------------------------------------------------------------------------
-// Mid-size GEMM (64 < M <= 128): 128-row tiles, with the workgroup's waves
+// Mid-size GEMM (48 < M <= 128): 128-row tiles, with the workgroup's waves
 // split by role so that no load is waited for early.  With this few rows the
 // weights come from HBM exactly once and a K-block computes briefly, so the
 // loads need several K-blocks of lead, and a wait on the vector-memory counter
@@ -524,6 +595,7 @@ constexpr int kMidD = 4;                                // weight ring slots
 constexpr int kMidSlot = kWr + 2 * kTileN;              // packed weights + fp16 weight scales
 constexpr int kMidStage = Geo<kMidTM>::A + 4 * kMidTM;  // codes + fp32 activation scales
 constexpr int kMidLds = 2 * kMidStage + kMidD * kMidSlot;
+static_assert(kMidTM * 136 * 2 <= kMidLds, "SwiGLU epilogue buffer fits in the mid kernel's LDS");
 constexpr int kMidVm = 5;  // direct loads per K-block and weight wave
 
 // Waves 0-3: packed weights of K-block g (16 KB, four 1 KB loads per wave, in
@@ -638,7 +710,7 @@ __device__ __forceinline__ void mid_loop(const GemmArgs& p, const LaneOffsets& o
   }
 }
 
-template <bool DIAG>
+template <bool DIAG, bool SWIGLU>
 __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
   constexpr int TM = kMidTM, kRB = Geo<TM>::RB;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -681,7 +753,7 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
     mid_loop<DIAG, true>(p, o, smem, lds, split, ge, gb, ge, NG, m0, n0, st, C);
     if (DIAG) continue;
 
-    store_tile<TM>(p, unit, m0, n0, C, &s_last);
+    store_tile<TM, SWIGLU>(p, unit, m0, n0, C, &s_last, smem);
   }
 }
 
@@ -689,30 +761,36 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
 
 int gemm_lds_bytes(int tile_m) { return tile_m == kMidTM ? kMidLds : Geo<256>::Lds; }
 
-hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, int tile_m,
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, int tile_m,
                        hipStream_t stream) {
   const dim3 grid(num_wgs), block(kThreads);
   if (tile_m == kMidTM) {
     if (diag)
-      hipLaunchKernelGGL(gemm_mid_kernel<true>, grid, block, kMidLds, stream, a);
+      hipLaunchKernelGGL((gemm_mid_kernel<true, false>), grid, block, kMidLds, stream, a);
+    else if (swiglu)
+      hipLaunchKernelGGL((gemm_mid_kernel<false, true>), grid, block, kMidLds, stream, a);
     else
-      hipLaunchKernelGGL(gemm_mid_kernel<false>, grid, block, kMidLds, stream, a);
+      hipLaunchKernelGGL((gemm_mid_kernel<false, false>), grid, block, kMidLds, stream, a);
   } else {
     if (diag)
-      hipLaunchKernelGGL((gemm_kernel<256, true>), grid, block, Geo<256>::Lds, stream, a);
+      hipLaunchKernelGGL((gemm_kernel<256, true, false>), grid, block, Geo<256>::Lds, stream, a);
+    else if (swiglu)
+      hipLaunchKernelGGL((gemm_kernel<256, false, true>), grid, block, Geo<256>::Lds, stream, a);
     else
-      hipLaunchKernelGGL((gemm_kernel<256, false>), grid, block, Geo<256>::Lds, stream, a);
+      hipLaunchKernelGGL((gemm_kernel<256, false, false>), grid, block, Geo<256>::Lds, stream, a);
   }
   return hipGetLastError();
 }
 
 hipError_t set_gemm_attributes() {
-  const void* fns[4] = {reinterpret_cast<const void*>(&gemm_kernel<256, false>),
-                        reinterpret_cast<const void*>(&gemm_kernel<256, true>),
-                        reinterpret_cast<const void*>(&gemm_mid_kernel<false>),
-                        reinterpret_cast<const void*>(&gemm_mid_kernel<true>)};
-  const int lds[4] = {Geo<256>::Lds, Geo<256>::Lds, kMidLds, kMidLds};
-  for (int i = 0; i < 4; ++i) {
+  const void* fns[6] = {reinterpret_cast<const void*>(&gemm_kernel<256, false, false>),
+                        reinterpret_cast<const void*>(&gemm_kernel<256, true, false>),
+                        reinterpret_cast<const void*>(&gemm_kernel<256, false, true>),
+                        reinterpret_cast<const void*>(&gemm_mid_kernel<false, false>),
+                        reinterpret_cast<const void*>(&gemm_mid_kernel<true, false>),
+                        reinterpret_cast<const void*>(&gemm_mid_kernel<false, true>)};
+  const int lds[6] = {Geo<256>::Lds, Geo<256>::Lds, Geo<256>::Lds, kMidLds, kMidLds, kMidLds};
+  for (int i = 0; i < 6; ++i) {
     hipError_t e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, lds[i]);
     if (e != hipSuccess) return e;
   }

@@ -46,6 +46,12 @@ struct GemmArgs {
   int splits;         // split-K slots per column block (few-token kernel)
   int win_m0, win_m1, win_n0, win_n1;
   BlockMap map;
+  // SwiGLU epilogue (tile and mid kernels): h of tile column block j goes,
+  // quantized with out_map, to block j of out_A (block-major, M rows) and
+  // out_sa [N/256][M]; nothing is written to `out`
+  uint8_t* out_A;
+  uint16_t* out_sa;
+  BlockMap out_map;
 };
 
 // perm == nullptr: no channel permutation.
@@ -74,8 +80,13 @@ constexpr int kTileN = 256;
 inline int gemm_tile_m(int M) { return M <= kTileMSmall ? kTileMSmall : kTileM; }
 
 // Persistent GEMM: `num_wgs` workgroups walk a.units (a.wg_begin per group);
-// tile_m is gemm_tile_m(a.M).
-hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, int tile_m, hipStream_t stream);
+// tile_m is gemm_tile_m(a.M); swiglu selects the SwiGLU + quantize epilogue.
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, int tile_m,
+                       hipStream_t stream);
+// SwiGLU of an fp16 gate/up output GU [M][2I] (2G-wide gate/up column groups)
+// and FMPQ quantization of h [M][I] with `map` into A / sa [I/G][M].
+hipError_t launch_swiglu_quantize(const uint16_t* GU, uint8_t* A, uint16_t* sa, int M, int I,
+                                  const BlockMap& map, hipStream_t stream);
 // Few-token kernel (M <= kSkinnyMaxM): one wave per (16 columns, split-K slot).
 constexpr int kSkinnyMaxM = 48;
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);

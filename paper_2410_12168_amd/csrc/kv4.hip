@@ -13,7 +13,7 @@
 //
 // The division (x - mn) / s uses one correctly rounded reciprocal per lane and
 // Markstein's correction step (two fmas per element), exact for a binary16 s;
-// quantize.hip gives the argument.
+// fmpq.h gives the argument.
 //
 // Work decomposition: a lane owns 8 consecutive channels (one 16-byte load);
 // G/8 lanes share a group and reduce min/max with xor shuffles.  Groups are

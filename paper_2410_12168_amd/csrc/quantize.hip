@@ -11,21 +11,7 @@
 // The activation grid is 2-D (block, row group): no 64-bit index division.
 // 2 bytes in per channel, 0.5 or 1 byte out.
 //
-// Division.  The codes need RN(x / s) exactly (IEEE fp32 division), which as
-// a library division costs about ten vector instructions per element and made
-// these kernels ALU-bound.  Instead each lane takes one correctly rounded
-// reciprocal r = RN(1/s) and per element
-//     q0 = RN(x r),  rem = x - q0 s  (one fma, exact),  q = RN(q0 + rem r),
-// Markstein's correction step.  Why q = RN(x / s) here: s is a binary16
-// value, so its significand has at most 11 bits.  q0 is within 2 ulps of x/s,
-// so rem is a multiple of ulp(q0) * 2^e(s) of at most 13 bits: exact.  The
-// fma then sees x/s perturbed by at most |rem| |r - 1/s| <= 2^-46 ulp-units
-// of the result, while x/s, when it is not a midpoint between binary32
-// neighbours, lies at least 2^-35 units from one (x has 24 bits, s 11 bits),
-// and it is never exactly a midpoint (a midpoint needs 25 significant bits
-// times s's odd part).  So rounding the perturbed value gives RN(x / s).  The
-// identity is also checked exhaustively over every binary16 operand pair on
-// the CPU.  s == 0 takes r = 0, which yields q = 0 as the quantizer requires.
+// Division: see fmpq.h.
 //
 // Channel permutation (Sec. 3.2): with a permutation the lane reads its 8
 // channels X[m][perm[c]]: one vector load where the permutation leaves the
@@ -39,77 +25,13 @@
 
 #include <algorithm>
 
+#include "fmpq.h"
 #include "kernels.h"
+#include "swiglu.h"
 
 namespace comet {
 
 namespace {
-
-struct Codes {
-  uint32_t sign[8];
-  uint32_t mag[8];
-};
-
-// Quantize the 8 channels this lane holds, given the block-wide max |x|.
-// Scale and codes follow the block quantizer exactly: one IEEE fp32 division
-// for the scale, rounding to binary16 (nearest even), then one IEEE fp32
-// division per element, rint (nearest even) and clamp.
-// RN(a / s) from r = RN(1/s) for a binary16 s (see the header).
-__device__ inline float div_rn(float a, float s, float r) {
-  const float q0 = a * r;
-  const float rem = fmaf(-q0, s, a);
-  return fmaf(rem, r, q0);
-}
-
-// Magnitudes and signs follow q = clamp(rint(x / s), -qmax, qmax) with the
-// sign taken from x (rint and the division are symmetric); a zero code has a
-// clear sign bit.
-__device__ inline uint16_t quantize8(const float (&x)[8], float amax, float qmax, Codes& c) {
-  float s32 = amax / qmax;
-  __half h = __float2half_rn(s32);
-  float s = __half2float(h);
-  const float r = s != 0.0f ? 1.0f / s : 0.0f;
-  #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const float m = fminf(rintf(div_rn(fabsf(x[i]), s, r)), qmax);
-    c.mag[i] = (uint32_t)m;
-    c.sign[i] = (__float_as_uint(x[i]) >> 31) & (m != 0.0f ? 1u : 0u);
-  }
-  return __half_as_ushort(h);
-}
-
-// Sign-magnitude 4-bit codes of channels 0..7 into one dword.  Byte k:
-//   bit 7 = sign(k), bits 6..4 = |code 4+k|, bit 3 = sign(4+((k+3)&3)), bits 2..0 = |code k|,
-// so that (w & 0x87878787) and (rotr(w, 4) & 0x87878787) are FP8-E4M3 subnormals.
-__device__ inline uint32_t pack4(const Codes& c) {
-  uint32_t w = 0;
-  #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    uint32_t b = (c.sign[k] << 7) | (c.mag[4 + k] << 4) | (c.sign[4 + ((k + 3) & 3)] << 3) | c.mag[k];
-    w |= b << (8 * k);
-  }
-  return w;
-}
-
-__device__ inline uint2 pack8(const Codes& c) {
-  uint32_t w0 = 0, w1 = 0;
-  #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    w0 |= ((c.sign[k] << 7) | c.mag[k]) << (8 * k);
-    w1 |= ((c.sign[4 + k] << 7) | c.mag[4 + k]) << (8 * k);
-  }
-  return make_uint2(w0, w1);
-}
-
-__device__ inline void load8(const uint16_t* p, float (&x)[8]) {
-  uint4 v = *reinterpret_cast<const uint4*>(p);
-  uint32_t w[4] = {v.x, v.y, v.z, v.w};
-  #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    x[2 * i] = __half2float(__ushort_as_half((unsigned short)(w[i] & 0xFFFF)));
-    x[2 * i + 1] = __half2float(__ushort_as_half((unsigned short)(w[i] >> 16)));
-  }
-}
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -144,22 +66,6 @@ __device__ inline void gather8(const uint16_t* row, const uint32_t (&idx)[8], in
   const uint32_t last = (uint32_t)(K - 1);
   #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = __half2float(__ushort_as_half(row[min(idx[i], last)]));
-}
-
-__device__ inline float max16(float v) {
-  // butterfly over the 16 lanes of one (row, block) pair
-  v = fmaxf(v, __shfl_xor(v, 1, 16));
-  v = fmaxf(v, __shfl_xor(v, 2, 16));
-  v = fmaxf(v, __shfl_xor(v, 4, 16));
-  v = fmaxf(v, __shfl_xor(v, 8, 16));
-  return v;
-}
-
-__device__ inline int n8_before(const BlockMap& map, int g) {
-  int n = 0;
-  for (int w = 0; w < (g >> 6); ++w) n += __popcll(map.bits[w]);
-  if (g & 63) n += __popcll(map.bits[g >> 6] & ((1ull << (g & 63)) - 1));
-  return n;
 }
 
 // Activations.  A workgroup owns one block g and 16 * R consecutive rows;
@@ -289,7 +195,55 @@ __global__ __launch_bounds__(256) void channel_absmax_kernel(const uint16_t* __r
   }
 }
 
+// SwiGLU + next-layer quantization of an fp16 gate/up output: workgroup
+// (x, y) = (block j, 32 rows from 32 y); 16 lanes own one (row, block) pair
+// and read 8 gate and 8 up values (two 16-byte loads), form h and quantize it
+// as the activation quantizer does.
+__global__ __launch_bounds__(256) void swiglu_quantize_kernel(const uint16_t* __restrict__ GU,
+                                                              uint8_t* __restrict__ A,
+                                                              uint16_t* __restrict__ sa, int M,
+                                                              int I, BlockMap map) {
+  const int lane16 = threadIdx.x & 15;
+  const int j = blockIdx.x;
+  const bool b8 = (map.bits[j >> 6] >> (j & 63)) & 1;
+  const size_t base = (size_t)M * 64 * (size_t)(j + n8_before(map, j));
+  #pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int m = blockIdx.y * 32 + 16 * t + (threadIdx.x >> 4);
+    const uint16_t* row = GU + (size_t)min(m, M - 1) * 2 * I + (size_t)j * 2 * kG + 8 * lane16;
+    const uint4 gv = *reinterpret_cast<const uint4*>(row);
+    const uint4 uv = *reinterpret_cast<const uint4*>(row + kG);
+    const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w}, uw[4] = {uv.x, uv.y, uv.z, uv.w};
+    float x[8];
+    #pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint16_t g = (uint16_t)(gw[i >> 1] >> (16 * (i & 1)));
+      const uint16_t u = (uint16_t)(uw[i >> 1] >> (16 * (i & 1)));
+      x[i] = __half2float(__ushort_as_half(swiglu_f16(g, u)));
+    }
+    float a = 0.0f;
+    #pragma unroll
+    for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
+    a = max16(a);
+    Codes c;
+    const uint16_t s16 = quantize8(x, a, b8 ? 127.0f : 7.0f, c);
+    if (m >= M) continue;
+    if (b8)
+      *reinterpret_cast<uint2*>(A + base + (size_t)m * 128 + 8 * lane16) = pack8(c);
+    else
+      *reinterpret_cast<uint32_t*>(A + base + (size_t)m * 64 + 4 * lane16) = pack4(c);
+    if (lane16 == 0) sa[(size_t)j * M + m] = s16;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_swiglu_quantize(const uint16_t* GU, uint8_t* A, uint16_t* sa, int M, int I,
+                                  const BlockMap& map, hipStream_t stream) {
+  hipLaunchKernelGGL(swiglu_quantize_kernel, dim3((unsigned)(I / kG), (unsigned)((M + 31) / 32)),
+                     dim3(256), 0, stream, GU, A, sa, M, I, map);
+  return hipGetLastError();
+}
 
 hipError_t launch_quantize_act(const uint16_t* X, const int32_t* perm, uint8_t* A, uint16_t* sa,
                                int M, int K, const BlockMap& map, hipStream_t stream) {

@@ -101,6 +101,16 @@ def test_device_entry_points_check_arguments():
     assert L.comet_kv4_quantize(p(FAKE), p(FAKE + 2), p(FAKE), 4, 128, 128, None) == 1
     assert L.comet_kv4_dequantize(p(FAKE), p(FAKE), p(FAKE), 4, 256, 256, None) == 2
     assert L.comet_kv4_dequantize(p(FAKE), p(FAKE), None, 4, 256, 128, None) == 1
+    # SwiGLU entry points: N a multiple of 256, I of 128, aligned outputs
+    W = p(FAKE)
+    assert L.comet_w4ax_gemm_swiglu_quant(W, mp, W, W, W, 16, 384, 256, 128, mp, W, W, None) == 1
+    assert L.comet_w4ax_gemm_swiglu_quant(W, mp, W, W, W, 16, 512, 256, 128, mp, p(FAKE + 4), W,
+                                          None) == 1
+    assert L.comet_w4ax_gemm_swiglu_quant(W, mp, W, W, W, 16, 512, 256, 128, mp, None, W,
+                                          None) == 1
+    assert L.comet_swiglu_quantize(W, mp, W, W, 4, 200, 128, None) == 1
+    assert L.comet_swiglu_quantize(W, mp, W, W, 4, 256, 64, None) == 2
+    assert L.comet_swiglu_quantize(W, mp, W, W, 0, 256, 128, None) == 1
     # the activation quantizer's row limit
     assert L.comet_fmpq_quantize_act_perm(p(FAKE), None, mp, p(FAKE), p(FAKE), 65535 * 32 + 1, 256,
                                           128, None) == 2

@@ -202,3 +202,73 @@ def test_kv4_edge_values():
     assert np.array_equal(host_u16(params), p_ref)
     assert np.array_equal(host_u16(comet.kv4_dequantize(codes, params, G)),
                           oracle.kv4_dequantize(c_ref, p_ref, G))
+
+
+# --- SwiGLU + next-layer quantization ---------------------------------------------
+
+@pytest.mark.parametrize("M,I,kind", [(1, 128, "all4"), (7, 384, "random"), (100, 1024, "random"),
+                                      (33, 256, "all8")])
+def test_swiglu_quantize_bit_exact(M, I, kind):
+    print(f"swiglu_quantize M={M} I={I} {kind}", flush=True)
+    NG = I // 128
+    prec = {"all4": np.full(NG, 4, np.uint8), "all8": np.full(NG, 8, np.uint8),
+            "random": synth.prec_map(NG, max(1, NG // 3), "random", M)}[kind]
+    gu = synth.normal_fp16(M, 5, (M, 2 * I), 3.0)
+    gu[0, :16] = [0, 0x8000, 0x6000, 0xE000, 0x3C00, 0xBC00, 1, 0x8001,
+                  0x4900, 0xC900, 0x5640, 0xD640, 0x0400, 0x8400, 0x3555, 0xB555]
+    A, sa = comet.swiglu_quantize(dev_u16(gu), prec)
+    A_ref, sa_ref = oracle.swiglu_quantize(gu, prec)
+    assert np.array_equal(host_u16(sa), sa_ref)
+    assert np.array_equal(host(A), A_ref)
+
+
+def gemm_inputs(M, N, K, seed):
+    NG = K // 128
+    prec = synth.prec_map(NG, max(1, NG // 8))
+    X16 = synth.activations(seed, M, K, prec)
+    W16 = synth.weights(seed, N, K)
+    A, sa = comet.quantize_act(dev_u16(X16), prec)
+    Wp, sw = comet.pack_w4(dev_u16(W16))
+    return prec, A, sa, Wp, sw
+
+
+# few-token (two-step), 128-row tiles, 256-row tiles, split tiles (320 tiles)
+FUSED = [(8, 512, 1024), (100, 768, 1024), (300, 1024, 2048), (1024, 20480, 1024)]
+
+
+@pytest.mark.parametrize("M,N,K", FUSED)
+def test_fused_swiglu_matches_oracle_on_gemm_output(M, N, K):
+    """The fused epilogue's quantized h is bit-identical to the oracle's SwiGLU
+    quantization of the same GEMM's fp16 output (the plain entry point, same
+    schedule, so the same fp16 gate/up values)."""
+    print(f"fused swiglu M={M} N={N} K={K}", flush=True)
+    I = N // 2
+    prec, A, sa, Wp, sw = gemm_inputs(M, N, K, seed=M + N)
+    out_map = synth.prec_map(I // 128, max(1, I // 128 // 4), "random", seed=N)
+    A2, sa2 = comet.w4ax_gemm_swiglu_quant(A, prec, sa, Wp, sw, M, N, K, out_map)
+    out = comet.w4ax_gemm(A, prec, sa, Wp, sw, M, N, K)
+    gu = host_u16(out)
+    rows = np.arange(M) if M <= 300 else np.array([0, 1, 255, 256, 511, 777, M - 1])
+    A_ref, sa_ref = oracle.swiglu_quantize(gu[rows], out_map)
+    assert np.array_equal(host_u16(sa2)[:, rows], sa_ref)
+    assert np.array_equal(act_rows(host(A2), out_map, M, rows), A_ref)
+    # the standalone kernel on the same output agrees as well
+    A3, sa3 = comet.swiglu_quantize(out, out_map)
+    assert torch.equal(A2, A3) and torch.equal(sa2.view(torch.int16), sa3.view(torch.int16))
+
+
+def test_fused_swiglu_llama3_70b_gate_up_sampled_rows():
+    """LLaMA-3-70B gate_up (M = 4096, K = 8192 -> N = 2 x 28672) fused into the
+    down projection's input (I = 28672, 1/16 of its blocks 8-bit)."""
+    M, (K, N) = 4096, synth.LLAMA3_70B["gate_up"]
+    print(f"fused swiglu 70B M={M} N={N} K={K}", flush=True)
+    I = N // 2
+    prec, A, sa, Wp, sw = gemm_inputs(M, N, K, seed=70)
+    out_map = synth.prec_map(I // 128, I // 128 // 16)
+    A2, sa2 = comet.w4ax_gemm_swiglu_quant(A, prec, sa, Wp, sw, M, N, K, out_map)
+    out = comet.w4ax_gemm(A, prec, sa, Wp, sw, M, N, K)
+    rows = np.array([0, 1, 777, 2048, 4095])
+    gu = host_u16(out[torch.from_numpy(rows).to(DEV)])
+    A_ref, sa_ref = oracle.swiglu_quantize(gu, out_map)
+    assert np.array_equal(host_u16(sa2)[:, rows], sa_ref)
+    assert np.array_equal(act_rows(host(A2), out_map, M, rows), A_ref)
