@@ -23,11 +23,15 @@
 //     last wave of tiles is split over all of them by cost;
 //   * the tile's packed 4-bit weights stream HBM -> LDS with direct
 //     (register-free) 128-bit loads into a ring of three K-block slots,
-//     issued two K-blocks ahead; each wave unpacks the weight fragments it
-//     uses when it reads them;
-//   * the tile's activation codes and both scale vectors are staged
-//     HBM -> VGPR -> unpack -> LDS one K-block ahead (double-buffered, XOR
-//     swizzled rows), so activation nibbles are unpacked once per workgroup;
+//     issued two K-blocks ahead by waves 4-7; each wave unpacks the weight
+//     fragments it uses when it reads them;
+//   * the tile's activation codes stream HBM -> LDS one K-block ahead with
+//     direct loads by waves 0-3, which then unpack 4-bit codes once per
+//     workgroup into a double-buffered stage of FP8 bytes (XOR swizzled
+//     rows); 8-bit codes land in the stage directly.  Waves 0-3 also stage
+//     both scale vectors.  Waves 0-3 win issue arbitration over the waves
+//     that share their SIMDs, so their extra work runs while waves 4-7 finish
+//     computing;
 //   * one barrier per K-block separates the stages;
 //   * each wave computes a 128x64 quadrant: 8x4 MFMA blocks per K-block;
 //   * split tiles write fp32 partials; the last workgroup to finish a tile
@@ -62,7 +66,8 @@ struct Geo {
   static constexpr int A = TM * 128;               // LDS bytes of one A stage (fp8 or raw 8-bit codes)
   static constexpr int S = 4 * (TM + kTileN);      // LDS bytes of one stage's scales (fp32)
   static constexpr int Buf = A + S;                // one activation stage, double-buffered
-  static constexpr int Lds = 2 * Buf + 3 * kWr;
+  static constexpr int Raw = TM * 64;              // packed 4-bit codes of the next K-block
+  static constexpr int Lds = 2 * Buf + 3 * kWr + Raw;
   static_assert(TM == 256 || TM == 128, "tile heights");
   static_assert(TM * 136 * 2 <= Lds, "SwiGLU epilogue buffer fits in LDS");
 };
@@ -142,72 +147,11 @@ __device__ __forceinline__ int plan_at(const int* a, int i) {
 __device__ __forceinline__ int order_at(const GemmArgs& p, int i) { return plan_at(p.order, i); }
 
 // Registers holding one K-block's activation codes and a scale between load
-// and LDS store.
+// and LDS store (the mid-size kernel's activation waves).
 struct Stage {
   u32x4 a[4];
   uint32_t s;
 };
-
-// Global loads of one K-block's activation codes and scales for the tile at
-// (m0, n0).
-// Rows and columns are clamped into range, so edge tiles never read out of
-// bounds; clamped rows and columns compute values that are never stored.
-template <int TM>
-__device__ __forceinline__ void stage_load(const GemmArgs& p, const KBlock& kb, int m0, int n0,
-                                           Stage& st) {
-  constexpr int N4 = TM / 128, N8 = TM / 64;  // 16-byte loads per lane, 4-bit / 8-bit block
-  const int tid = threadIdx.x;
-  const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)kb.aoff;
-  // 4-bit block: lane chunk tid%4 of rows tid/4 + 128 i (i < N4), 64 bytes a row;
-  // 8-bit block: lane chunk tid%8 of rows tid/8 + 64 i (i < N8), 128 bytes a row.
-  // The first N4 loads only switch offsets (arithmetic select, so that the
-  // staging registers are not forced into memory by a branch merge).
-  const uint32_t b8 = kb.b8 ? 1u : 0u;
-  #pragma unroll
-  for (int i = 0; i < N4; ++i) {
-    const int r = b8 ? (tid >> 3) + 64 * i : (tid >> 2) + 128 * i;
-    const uint32_t row = (uint32_t)min(m0 + r, p.M - 1);
-    const uint32_t off = (row << (6 + b8)) + ((uint32_t)tid & (3u | (b8 << 2))) * 16u;
-    st.a[i] = *reinterpret_cast<const u32x4*>(A + off);
-  }
-  if (kb.b8) {
-    #pragma unroll
-    for (int i = N4; i < N8; ++i) {
-      const uint32_t row = (uint32_t)min(m0 + (tid >> 3) + 64 * i, p.M - 1);
-      st.a[i] = *reinterpret_cast<const u32x4*>(A + row * 128u + (tid & 7) * 16u);
-    }
-  }
-  if (tid < TM)
-    st.s = p.sa[(size_t)kb.g * p.M + min(m0 + tid, p.M - 1)];
-  else
-    st.s = p.sw[(size_t)kb.g * p.N + min(n0 + min(tid - TM, kTileN - 1), p.N - 1)];
-}
-
-template <int TM>
-__device__ __forceinline__ void stage_store(const Stage& st, bool b8, uint8_t* buf) {
-  constexpr int N4 = TM / 128, N8 = TM / 64;
-  const int tid = threadIdx.x;
-  const int st4a = swz(tid >> 2, 2 * (tid & 3)), st4b = swz(tid >> 2, 2 * (tid & 3) + 1);
-  const int st8 = swz(tid >> 3, tid & 7);
-  if (!b8) {
-    #pragma unroll
-    for (int i = 0; i < N4; ++i) {
-      u32x4 lo, hi;
-      unpack4(st.a[i], lo, hi);
-      *reinterpret_cast<u32x4*>(buf + st4a + i * 16384) = lo;
-      *reinterpret_cast<u32x4*>(buf + st4b + i * 16384) = hi;
-    }
-  } else {
-    #pragma unroll
-    for (int i = 0; i < N8; ++i) *reinterpret_cast<u32x4*>(buf + st8 + i * 8192) = st.a[i];
-  }
-  const float f = __half2float(__ushort_as_half((unsigned short)st.s));
-  float* scales = reinterpret_cast<float*>(buf + Geo<TM>::A);
-  if (tid < TM)
-    scales[tid] = f * kUnit;
-  else if (tid < TM + kTileN)
-    scales[sw_slot<TM>(tid - TM)] = f;
-}
 
 // Direct global -> LDS load of 16 bytes per lane: the wave's 64 chunks land
 // at LDS bytes lds .. lds + 1023, lane by lane.  Issued as inline assembly so
@@ -231,15 +175,140 @@ __device__ __forceinline__ const uint8_t* w_src(const GemmArgs& p, int g, int n0
   return p.W + ((size_t)panel * NG + g) * 1024 + (lane >> 2) * 64 + chunk * 16;
 }
 
-// Packed weights of K-block g for the tile's 256 columns into a ring slot:
-// 16 KB, two 1 KB wave loads per wave.
-__device__ __forceinline__ void dma_w(const GemmArgs& p, int g, int n0, uint32_t slot) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+// Direct load with a scalar base and a 32-bit per-lane byte offset.
+__device__ __forceinline__ void dma16s(const uint8_t* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(base), "s"(lds) : "m0");
+}
+
+// Weight loads of waves 4-7: wave 4 + w loads panels 4 w .. 4 w + 3 of the
+// tile (clamped to the last panel past N).  Per tile, the panels' bases;
+// per lane, the offset of its column and chunk slot within a 1 KB K-block
+// (the ring layout of wswz()).
+struct WPanels {
+  const uint8_t* b[4];
+};
+__device__ __forceinline__ WPanels w_panels(const GemmArgs& p, int n0) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) - 4;
+  const int NG = p.K / kG;
+  WPanels wp;
   #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int j = 2 * wave + i;
-    dma16(w_src(p, g, n0, j), slot + j * 1024);
+  for (int i = 0; i < 4; ++i)
+    wp.b[i] = p.W + (size_t)min(n0 / 16 + 4 * w + i, p.N / 16 - 1) * NG * 1024;
+  return wp;
+}
+__device__ __forceinline__ uint32_t w_lane_off() {
+  const int lane = threadIdx.x & 63;
+  return (lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) << 4);
+}
+
+// Packed weights of K-block g for the tile's 256 columns into a ring slot:
+// 16 KB, four 1 KB wave loads by each of waves 4-7.
+__device__ __forceinline__ void dma_w(const WPanels& wp, uint32_t voff, int g, uint32_t slot) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) - 4;
+  #pragma unroll
+  for (int i = 0; i < 4; ++i) dma16s(wp.b[i] + (size_t)g * 1024, voff, slot + (4 * w + i) * 1024);
+}
+
+// Activation codes of K-block kb for the tile's 256 rows, by waves 0-3 (wave
+// w: rows 64 w .. 64 w + 63), straight into LDS.  A 4-bit block lands packed
+// in the raw slot (row r at r * 64), to be unpacked by act_unpack; an 8-bit
+// block lands in activation stage `stage` in its final swizzled layout (LDS
+// chunk slot s of row r holds code chunk s ^ g(r)).  Rows past M re-read row
+// M - 1.
+// Load i (i < 4) of a 4-bit block: rows 64 w + 16 i .. + 15.  A is the block's
+// base; byte offsets within a block stay below 2^32 (at most 2^21 rows of
+// 128 bytes).
+__device__ __forceinline__ void act_dma4(const uint8_t* A, int M, int m0, int i, uint32_t raw) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = 64 * wave + 16 * i + (lane >> 2);
+  const uint32_t off = (uint32_t)min(m0 + r, M - 1) * 64u + (lane & 3) * 16u;
+  dma16s(A, off, raw + (4 * wave + i) * 1024);
+}
+// Load i (i < 8) of an 8-bit block: rows 64 w + 8 i .. + 7.
+__device__ __forceinline__ void act_dma8(const uint8_t* A, int M, int m0, int i, uint32_t stage) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = 64 * wave + 8 * i + (lane >> 3);
+  const int c = (lane & 7) ^ ((r ^ (r >> 1)) & 7);
+  const uint32_t off = (uint32_t)min(m0 + r, M - 1) * 128u + c * 16u;
+  dma16s(A, off, stage + (8 * wave + i) * 1024);
+}
+// Loads of a tile that lies inside M (m0 + 256 <= M): no row is clamped, so a
+// load is a scalar base and a per-lane constant.  4-bit load i of wave w
+// covers rows 64 w + 16 i .. + 15 (lane offset lane * 16); 8-bit load i rows
+// 64 w + 8 i .. + 7, whose swizzle depends on i only through i & 1 (lane
+// offsets a8[0], a8[1]).
+struct ActLane {
+  uint32_t a4, a8[2];
+};
+__device__ __forceinline__ ActLane act_lane() {
+  const int lane = threadIdx.x & 63;
+  ActLane l;
+  l.a4 = lane * 16;
+  #pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int r = 8 * h + (lane >> 3);  // row modulo 16
+    l.a8[h] = (lane >> 3) * 128 + (((lane & 7) ^ ((r ^ (r >> 1)) & 7)) << 4);
   }
+  return l;
+}
+__device__ __forceinline__ void act_dma4_in(const uint8_t* A, int m0, int i, const ActLane& l,
+                                            uint32_t raw) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  dma16s(A + (size_t)(m0 + 64 * wave) * 64 + i * 1024, l.a4, raw + (4 * wave + i) * 1024);
+}
+__device__ __forceinline__ void act_dma8_in(const uint8_t* A, int m0, int i, const ActLane& l,
+                                            uint32_t stage) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  dma16s(A + (size_t)(m0 + 64 * wave) * 128 + i * 1024, l.a8[i & 1],
+         stage + (8 * wave + i) * 1024);
+}
+
+__device__ __forceinline__ void act_dma(const GemmArgs& p, const KBlock& kb, int m0, uint32_t raw,
+                                        uint32_t stage) {
+  const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)kb.aoff;
+  if (!kb.b8) {
+    #pragma unroll
+    for (int i = 0; i < 4; ++i) act_dma4(A, p.M, m0, i, raw);
+  } else {
+    #pragma unroll
+    for (int i = 0; i < 8; ++i) act_dma8(A, p.M, m0, i, stage);
+  }
+}
+
+// Waves 0-3: unpack the 4-bit codes that this wave loaded into the raw slot
+// into activation stage `buf` (FP8 bytes, swizzled rows).
+__device__ __forceinline__ void act_unpack(const uint8_t* raw, uint8_t* buf) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  #pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 64 * wave + 16 * i + (lane >> 2), c = lane & 3;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(raw + (4 * wave + i) * 1024 + lane * 16);
+    u32x4 lo, hi;
+    unpack4(v, lo, hi);
+    *reinterpret_cast<u32x4*>(buf + swz(r, 2 * c)) = lo;
+    *reinterpret_cast<u32x4*>(buf + swz(r, 2 * c + 1)) = hi;
+  }
+}
+
+// Waves 0-3 (thread t): the fp16 scales of tile row t and tile column t for
+// K-block g, loaded ahead into registers and stored as fp32 into a stage.
+struct StageScales {
+  uint32_t sa, sw;  // zero-extended fp16 bits, kept apart so that no wait is forced at the load
+};
+__device__ __forceinline__ StageScales scales_load(const GemmArgs& p, int g, int m0, int n0) {
+  const int t = threadIdx.x;
+  return StageScales{(uint32_t)p.sa[(size_t)g * p.M + min(m0 + t, p.M - 1)],
+                     (uint32_t)p.sw[(size_t)g * p.N + min(n0 + t, p.N - 1)]};
+}
+template <int TM>
+__device__ __forceinline__ void scales_store(StageScales sc, uint8_t* buf) {
+  const int t = threadIdx.x;
+  float* scales = reinterpret_cast<float*>(buf + Geo<TM>::A);
+  scales[t] = __half2float(__ushort_as_half((unsigned short)sc.sa)) * kUnit;
+  scales[sw_slot<TM>(t)] = __half2float(__ushort_as_half((unsigned short)sc.sw));
 }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -273,11 +342,18 @@ __device__ __forceinline__ f32x4 stage_sw(const uint8_t* buf) {
 // One K-block of the wave's quadrant: activation stage `buf` (fp8 or raw
 // 8-bit codes, then activation scales), packed weights in ring slot `wbuf`,
 // the lane's weight scales in swl.
-template <int TM, bool DIAG, bool B8>
+struct NoHook {
+  __device__ void operator()(int) const {}
+};
+
+// hook(s) runs after the MFMA issue of step s (s < RB * 4): loads spread over
+// the K-block instead of issued in one burst.
+template <int TM, bool DIAG, bool B8, class Hook = NoHook>
 __device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t* wbuf, f32x4 swl,
                                               const LaneOffsets& o, int g, int NG, int m0, int n0,
                                               const GemmArgs& p,
-                                              f32x4 (&C)[Geo<TM>::RB][kCB]) {
+                                              f32x4 (&C)[Geo<TM>::RB][kCB],
+                                              Hook&& hook = NoHook()) {
   constexpr int kRB = Geo<TM>::RB;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -318,6 +394,7 @@ __device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t*
     f32x4 y = mfma_fp8(af, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
     f32x4 yh;
     if constexpr (B8) yh = mfma_fp8(ah, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
+    hook(s);
     if (cb == kCB - 1 && rb + 1 < kRB) {
       // the next row block's fragment replaces this one in the same registers
       __builtin_amdgcn_sched_barrier(0);
@@ -365,33 +442,79 @@ __device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t*
 
 // Pipelined K-loop over schedule positions [pos, end), all of precision B8.
 // Relative position j = pos - g_begin computes from activation stage j % 2
-// and weight ring slot j % 3.  During it, the activation stage of j + 1 is
-// loaded into registers and stored to the other stage, and the weights of
-// j + 2 are loaded straight into ring slot (j + 2) % 3, last read at j - 1.
-// The weights of j + 1 were issued before this iteration's activation loads,
-// so they have arrived once those have (loads complete in order); the wait
-// before the barrier makes that explicit.
+// and weight ring slot j % 3.  The waves split the loads by role:
+//   * waves 0-3 load the scales of j + 1 and start the direct loads of its
+//     activation codes (into the raw slot, or for an 8-bit block into stage
+//     (j + 1) % 2, read last at j - 1), compute j, then wait for their own
+//     loads and unpack the codes into stage (j + 1) % 2.  They are the waves
+//     that win issue arbitration, so this work runs while waves 4-7 still
+//     compute;
+//   * waves 4-7 start the direct loads of the weights of j + 2 into ring slot
+//     (j + 2) % 3 (read last at j - 1), compute j, and wait only for the
+//     weights of j + 1 (loads complete in order: at most the four of j + 2
+//     stay in flight).
+// The direct loads are issued a few MFMA steps into the K-block, those of
+// waves 4-7 one step before those of waves 0-3: issued at the top all at once
+// they queue for the memory pipeline, and the waves wait for the issue with
+// idle matrix cores.  Tiles that cross M (clamped rows) issue their activation
+// loads at the top.  One barrier per K-block publishes the stage and the
+// weights.
 template <int TM, bool DIAG, bool B8>
 __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o, uint8_t* smem,
-                                      uint32_t lds, int g_begin, int pos, int end, int g_end,
-                                      int NG, int m0, int n0, Stage& st,
+                                      uint32_t lds, const int* order, int g_begin, int pos,
+                                      int end, int g_end, int NG, int m0, int n0,
+                                      const WPanels& wp, uint32_t wvoff,
                                       f32x4 (&C)[Geo<TM>::RB][kCB]) {
-  constexpr int kBuf = Geo<TM>::Buf;
+  constexpr int kBuf = Geo<TM>::Buf, kRaw = 2 * kBuf + 3 * kWr;
+  const bool awave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4;
+  const bool inside = m0 + TM <= p.M;
+  const ActLane al = act_lane();
+  // schedule entries of pos, pos + 1 and pos + 2 (clamped to the unit),
+  // each read from the LDS copy one K-block ahead
+  int e0 = order[pos], e1 = order[min(pos + 1, g_end - 1)], e2 = order[min(pos + 2, g_end - 1)];
   for (; pos < end; ++pos) {
     const int j = pos - g_begin;
     const int cur = j & 1, wslot = j % 3;
-    const bool more = pos + 1 < g_end;
-    const KBlock kb = kblock(order_at(p, pos));
-    const KBlock kn = kblock(order_at(p, more ? pos + 1 : pos));
-    if (more) stage_load<TM>(p, kn, m0, n0, st);
-    compute_block<TM, DIAG, B8>(smem + cur * kBuf, smem + 2 * kBuf + wslot * kWr,
-                                stage_sw<TM>(smem + cur * kBuf), o, kb.g, NG, m0, n0, p, C);
-    if (more) stage_store<TM>(st, kn.b8, smem + (cur ^ 1) * kBuf);
-    wait_vm_all();
-    if (pos + 2 < g_end) {
-      const int nslot = wslot == 0 ? 2 : wslot - 1;  // (j + 2) % 3
-      dma_w(p, kblock(order_at(p, pos + 2)).g, n0, lds + 2 * kBuf + nslot * kWr);
+    const bool more = pos + 1 < g_end, wnext = pos + 2 < g_end;
+    const KBlock kb = kblock(__builtin_amdgcn_readfirstlane(e0));
+    const KBlock kn = kblock(__builtin_amdgcn_readfirstlane(e1));
+    const int g2 = kblock(__builtin_amdgcn_readfirstlane(e2)).g;
+    StageScales sc;
+    const int e3 = order[min(pos + 3, g_end - 1)];
+    const uint8_t* Anext = p.A + (size_t)p.M * 64 * (size_t)kn.aoff;
+    const uint32_t wdst = lds + 2 * kBuf + (wslot == 0 ? 2 : wslot - 1) * kWr;  // slot (j + 2) % 3
+    if (awave && more) {
+      sc = scales_load(p, kn.g, m0, n0);
+      if (!inside) act_dma(p, kn, m0, lds + kRaw, lds + (cur ^ 1) * kBuf);
     }
+    auto hook = [&](int s) {
+      if (s == 2 && !awave && wnext) dma_w(wp, wvoff, g2, wdst);
+      if (s == 3 && awave && more && inside) {
+        if (!kn.b8) {
+          #pragma unroll
+          for (int i = 0; i < 4; ++i) act_dma4_in(Anext, m0, i, al, lds + kRaw);
+        } else {
+          #pragma unroll
+          for (int i = 0; i < 8; ++i) act_dma8_in(Anext, m0, i, al, lds + (cur ^ 1) * kBuf);
+        }
+      }
+    };
+    compute_block<TM, DIAG, B8>(smem + cur * kBuf, smem + 2 * kBuf + wslot * kWr,
+                                stage_sw<TM>(smem + cur * kBuf), o, kb.g, NG, m0, n0, p, C, hook);
+    if (awave) {
+      if (more) {
+        wait_vm_all();
+        if (!kn.b8) act_unpack(smem + kRaw, smem + (cur ^ 1) * kBuf);
+        scales_store<TM>(sc, smem + (cur ^ 1) * kBuf);
+      }
+    } else if (wnext) {
+      asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    } else {
+      wait_vm_all();
+    }
+    e0 = e1;
+    e1 = e2;
+    e2 = e3;
     barrier_lds();
   }
 }
@@ -534,10 +657,14 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
   constexpr int kRB = Geo<TM>::RB, kBuf = Geo<TM>::Buf;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int s_last;
+  __shared__ int s_order[kMaxBlocks];
   const int NG = p.K / kG;
   const LaneOffsets o = lane_offsets<TM>();
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
   const int u_end = plan_at(p.wg_begin, blockIdx.x + 1);
+  for (int i = threadIdx.x; i < NG; i += kThreads) s_order[i] = p.order[i];
+  __syncthreads();
+  const uint32_t wvoff = w_lane_off();
 
   for (int u = plan_at(p.wg_begin, blockIdx.x); u < u_end; ++u) {
     const int* ue = reinterpret_cast<const int*>(p.units) + 5 * u;
@@ -554,20 +681,31 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 
     // software pipeline over the unit's K-blocks; the schedule lists all
     // 4-bit blocks before the 8-bit ones, so each precision runs its own loop
-    Stage st;
     const KBlock k0 = kblock(order_at(p, unit.g_begin));
-    dma_w(p, k0.g, n0, lds + 2 * kBuf);
-    if (unit.g_begin + 1 < unit.g_end)
-      dma_w(p, kblock(order_at(p, unit.g_begin + 1)).g, n0, lds + 2 * kBuf + kWr);
-    stage_load<TM>(p, k0, m0, n0, st);
-    stage_store<TM>(st, k0.b8, smem);
-    wait_vm_all();
+    const WPanels wp = w_panels(p, n0);
+    if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4) {
+      act_dma(p, k0, m0, lds + 2 * kBuf + 3 * kWr, lds);
+      const StageScales sc = scales_load(p, k0.g, m0, n0);
+      wait_vm_all();
+      if (!k0.b8) act_unpack(smem + 2 * kBuf + 3 * kWr, smem);
+      scales_store<TM>(sc, smem);
+    } else {
+      dma_w(wp, wvoff, k0.g, lds + 2 * kBuf);
+      if (unit.g_begin + 1 < unit.g_end) {
+        dma_w(wp, wvoff, kblock(order_at(p, unit.g_begin + 1)).g, lds + 2 * kBuf + kWr);
+        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+      } else {
+        wait_vm_all();
+      }
+    }
     barrier_lds();
     const int split = min(max(p.n4, unit.g_begin), unit.g_end);
-    kloop<TM, DIAG, false>(p, o, smem, lds, unit.g_begin, unit.g_begin, split, unit.g_end, NG,
-                           m0, n0, st, C);
-    kloop<TM, DIAG, true>(p, o, smem, lds, unit.g_begin, split, unit.g_end, unit.g_end, NG, m0,
-                          n0, st, C);
+    if (unit.g_begin < split)
+      kloop<TM, DIAG, false>(p, o, smem, lds, s_order, unit.g_begin, unit.g_begin, split,
+                             unit.g_end, NG, m0, n0, wp, wvoff, C);
+    if (split < unit.g_end)
+      kloop<TM, DIAG, true>(p, o, smem, lds, s_order, unit.g_begin, split, unit.g_end, unit.g_end,
+                            NG, m0, n0, wp, wvoff, C);
     if (DIAG) continue;
 
     store_tile<TM, SWIGLU>(p, unit, m0, n0, C, &s_last, smem);
