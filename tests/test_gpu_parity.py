@@ -171,6 +171,16 @@ SKINNY = [
     (8, 512, 2048, "random"),
     (16, 256, 4096, "cfg0"),
     (40, 128, 2048, "all8"),
+    # 8 < M <= 32 (activation operand shared through LDS): ragged M; column
+    # blocks that leave the last workgroup partly idle; K-blocks that split
+    # unevenly over two slots (9 blocks: 4 + 5, so one slot runs dead steps)
+    (9, 80, 1152, "random"),
+    (17, 208, 2048, "alternate"),
+    (24, 1040, 4096, "cfg0"),
+    (31, 336, 1536, "all8"),
+    # two split-K slots (N = 8192) with uneven halves: 4 + 5 and 8 + 9 blocks
+    (20, 8192, 1152, "random"),
+    (12, 8192, 2176, "alternate"),
 ]
 
 
