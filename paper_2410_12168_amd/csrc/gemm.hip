@@ -728,6 +728,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 //     double-buffered LDS stage;
 //   * all eight waves compute their 64 x 64 quadrant with the tile kernel's
 //     K-block step.
+// As in the tile kernel, both roles issue their loads a few MFMA steps into
+// the K-block (not in a burst at its top), and the K-block order is read
+// from an LDS copy.
 constexpr int kMidTM = 128;
 constexpr int kMidD = 4;                                // weight ring slots
 constexpr int kMidSlot = kWr + 2 * kTileN;              // packed weights + fp16 weight scales
@@ -817,29 +820,29 @@ __device__ __forceinline__ void mid_store(const Stage& st, bool b8, uint8_t* buf
         __half2float(__ushort_as_half((unsigned short)st.s)) * kUnit;
 }
 
-// One K-block position of the mid-size loop: weights of pos + 3 issued,
-// activations of pos + 1 loaded and stored to the other stage.
+// One K-block position of the mid-size loop: weights of pos + 3 issued after
+// MFMA step 2, activations of pos + 1 loaded after step 3 and stored to the
+// other stage after the compute.
 template <bool DIAG, bool B8>
 __device__ __forceinline__ void mid_loop(const GemmArgs& p, const LaneOffsets& o, uint8_t* smem,
-                                         uint32_t lds, int pos, int end, int gb, int ge, int NG,
-                                         int m0, int n0, Stage& st,
+                                         uint32_t lds, const int* order, int pos, int end, int gb,
+                                         int ge, int NG, int m0, int n0, Stage& st,
                                          f32x4 (&C)[Geo<kMidTM>::RB][kCB]) {
-  const bool wwave = threadIdx.x < 256;
+  const bool wwave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4;
   for (; pos < end; ++pos) {
     const int j = pos - gb;
-    const KBlock kb = kblock(order_at(p, pos));
+    const KBlock kb = kblock(__builtin_amdgcn_readfirstlane(order[pos]));
     const bool more = pos + 1 < ge;
-    const KBlock kn = kblock(order_at(p, more ? pos + 1 : pos));
+    const KBlock kn = kblock(__builtin_amdgcn_readfirstlane(order[more ? pos + 1 : pos]));
+    const int g3 = kblock(__builtin_amdgcn_readfirstlane(order[min(pos + 3, ge - 1)])).g;
     const uint8_t* slot = smem + 2 * kMidStage + (j & 3) * kMidSlot;
-    if (wwave) {
-      if (pos + 3 < ge)
-        mid_dma(p, kblock(order_at(p, pos + 3)).g, n0,
-                lds + 2 * kMidStage + ((j + 3) & 3) * kMidSlot);
-    } else if (more) {
-      mid_load(p, kn, m0, st);
-    }
+    auto hook = [&](int s) {
+      if (s == 2 && wwave && pos + 3 < ge)
+        mid_dma(p, g3, n0, lds + 2 * kMidStage + ((j + 3) & 3) * kMidSlot);
+      if (s == 3 && !wwave && more) mid_load(p, kn, m0, st);
+    };
     compute_block<kMidTM, DIAG, B8>(smem + (j & 1) * kMidStage, slot, slot_sw(slot), o, kb.g, NG,
-                                    m0, n0, p, C);
+                                    m0, n0, p, C, hook);
     if (wwave)
       mid_wait(kMidVm * min(max(ge - pos - 2, 0), 2));
     else if (more)
@@ -853,11 +856,14 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
   constexpr int TM = kMidTM, kRB = Geo<TM>::RB;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int s_last;
+  __shared__ int s_order[kMaxBlocks];
   const int NG = p.K / kG;
   const LaneOffsets o = lane_offsets<TM>();
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
   const bool wwave = threadIdx.x < 256;
   const int u_end = plan_at(p.wg_begin, blockIdx.x + 1);
+  for (int i = threadIdx.x; i < NG; i += kThreads) s_order[i] = p.order[i];
+  __syncthreads();
 
   for (int u = plan_at(p.wg_begin, blockIdx.x); u < u_end; ++u) {
     const int* ue = reinterpret_cast<const int*>(p.units) + 5 * u;
@@ -887,8 +893,8 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
     }
     barrier_lds();
     const int split = min(max(p.n4, gb), ge);
-    mid_loop<DIAG, false>(p, o, smem, lds, gb, split, gb, ge, NG, m0, n0, st, C);
-    mid_loop<DIAG, true>(p, o, smem, lds, split, ge, gb, ge, NG, m0, n0, st, C);
+    if (gb < split) mid_loop<DIAG, false>(p, o, smem, lds, s_order, gb, split, gb, ge, NG, m0, n0, st, C);
+    if (split < ge) mid_loop<DIAG, true>(p, o, smem, lds, s_order, split, ge, gb, ge, NG, m0, n0, st, C);
     if (DIAG) continue;
 
     store_tile<TM, SWIGLU>(p, unit, m0, n0, C, &s_last, smem);
