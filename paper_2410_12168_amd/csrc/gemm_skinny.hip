@@ -98,14 +98,17 @@ __device__ __forceinline__ void load_scales(const GemmArgs& p, int gb, int n0, S
 
 // Weight fragments of the batch starting at K-block gb for the wave's panel
 // (rows n0 .. n0 + 15): load i is K-block gb + i, lane r + 16 q reading row
-// r's 16-byte chunk q.  K-blocks past the last one repeat it (never computed).
-__device__ __forceinline__ void load_w(const GemmArgs& p, int gb, int n0, u32x4 (&w)[4]) {
+// r's 16-byte chunk q.  K-blocks past glast (the slot's last block) repeat it:
+// they are never computed, and the repeat is a cache hit, where reading on
+// into the next slot's blocks would fetch them from HBM a second time.
+__device__ __forceinline__ void load_w(const GemmArgs& p, int gb, int glast, int n0,
+                                       u32x4 (&w)[4]) {
   const int lane = threadIdx.x & 63;
   const int NG = p.K / kG;
   const uint8_t* panel = p.W + (size_t)(n0 / 16) * NG * 1024 + (lane & 15) * 64 + (lane >> 4) * 16;
   #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int g = min(gb + i, NG - 1);
+    const int g = min(gb + i, glast);
     w[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(panel + (size_t)g * 1024));
   }
 }
@@ -187,7 +190,7 @@ __device__ __forceinline__ void batch(const GemmArgs& p, int gb, int g1, int n0,
                                       const SBatch<R>& sc, SBatch<R>& sn, AStep<R>& x,
                                       AStep<R>& y, f32x4 (&C)[R]) {
   const int NG = p.K / kG;
-  load_w(p, gb + kD, n0, wn);
+  load_w(p, gb + kD, g1 - 1, n0, wn);
   load_scales<R>(p, gb + kD, n0, sn);
   #pragma unroll
   for (int i = 0; i < kD; ++i) {
@@ -235,7 +238,7 @@ __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
     SBatch<R> sa_, sb_;
     AStep<R> x, y;
     int aoff = aoff_of(p, g0);
-    load_w(p, g0, n0, wa);
+    load_w(p, g0, g1 - 1, n0, wa);
     load_scales<R>(p, g0, n0, sa_);
     load_a<R>(p, g0, aoff, col, x);
     for (int gb = g0;;) {
@@ -427,7 +430,7 @@ __global__ __launch_bounds__(kCBW * S * 64) void skinny_shared_kernel(GemmArgs p
   // prologue: batch 0's activations stored, its weights and scales in flight
   chunk_load<R>(p, min(g0 + wi, NG - 1), ch);
   load_scales<R>(p, g0, n0, sa_);
-  load_w(p, g0, n0, wa);
+  load_w(p, g0, g1 - 1, n0, wa);
   chunk_store<R>(ch, area(0, wi));
   __syncthreads();
   // One batch b from weights wc and scales sc.  With NEXT, the next batch's
@@ -441,7 +444,7 @@ __global__ __launch_bounds__(kCBW * S * 64) void skinny_shared_kernel(GemmArgs p
     if constexpr (NEXT) {
       chunk_load<R>(p, min(gb + kD + wi, NG - 1), ch);
       load_scales<R>(p, gb + kD, n0, sn);
-      load_w(p, gb + kD, n0, wn);
+      load_w(p, gb + kD, g1 - 1, n0, wn);
     }
     issue_point();
     #pragma unroll
