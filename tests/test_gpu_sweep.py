@@ -50,3 +50,18 @@ def test_sweep_matches_oracle(M, N, K, kind):
     assert np.array_equal(host(r["acc"]), oracle.group_acc(qa[win[0]:win[1]], qw[win[2]:win[3]]))
     ref = oracle.dequant_gemm(qa, sa, qw, sw)
     assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"sweep {M}x{N}x{K}/{kind}")
+
+
+@pytest.mark.parametrize("M", [1, 20, 100, 300])
+def test_largest_k(M):
+    # K = 65536 (512 blocks, the most the block map holds) in every kernel
+    # regime: the K-block order table of the tile and mid-size kernels is full
+    N, K = 64, 65536
+    prec = make_map("random", K // 128, seed=M)
+    win = (max(0, M - 8), M, N - 16, N)
+    r = run_path(M, N, K, prec, seed=7 * M + 1, diag_window=win)
+    qa, sa = oracle.quantize_act(r["X16"], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    assert np.array_equal(host(r["acc"]), oracle.group_acc(qa[win[0]:win[1]], qw[win[2]:win[3]]))
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"largest K, M={M}")
