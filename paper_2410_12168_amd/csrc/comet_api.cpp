@@ -237,6 +237,14 @@ comet_status_t get_workspace(int dev, hipStream_t stream, size_t partial_floats,
                              Workspace** out) {
   Workspace& ws = g_ws[{dev, stream}];
   if (partial_floats > ws.partial_floats || counters > ws.ncounters) {
+    // only the split buffers are replaced; the stream's fp16 buffer (tmp)
+    // stays as it is
+    auto drop_split = [&ws] {
+      ws.partials = nullptr;
+      ws.counters = nullptr;
+      ws.partial_floats = 0;
+      ws.ncounters = 0;
+    };
     if (ws.partials) {
       // the previous launch on this stream may still use them
       hipError_t e = hipStreamSynchronize(stream);
@@ -246,18 +254,19 @@ comet_status_t get_workspace(int dev, hipStream_t stream, size_t partial_floats,
     }
     const size_t nf = std::max(partial_floats, ws.partial_floats);
     const size_t nc = std::max(counters, ws.ncounters);
-    ws = Workspace{};
+    drop_split();
     if (std::getenv("COMET_TEST_FAIL_ALLOC")) return fail(COMET_ERR_OOM, "workspace allocation failed (forced)");
     hipError_t e = hipMalloc(&ws.partials, std::max<size_t>(nf, 1) * sizeof(float));
     if (e != hipSuccess) {
-      ws = Workspace{};
+      drop_split();
       return fail(COMET_ERR_OOM, "workspace allocation: %s", hipGetErrorString(e));
     }
     e = hipMalloc(&ws.counters, std::max<size_t>(nc, 1) * sizeof(int));
     if (e == hipSuccess) e = hipMemsetAsync(ws.counters, 0, std::max<size_t>(nc, 1) * sizeof(int), stream);
     if (e != hipSuccess) {
       (void)hipFree(ws.partials);
-      ws = Workspace{};
+      if (ws.counters) (void)hipFree(ws.counters);
+      drop_split();
       return fail(COMET_ERR_OOM, "workspace counters: %s", hipGetErrorString(e));
     }
     ws.partial_floats = nf;

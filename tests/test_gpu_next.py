@@ -272,3 +272,34 @@ def test_fused_swiglu_llama3_70b_gate_up_sampled_rows():
     A_ref, sa_ref = oracle.swiglu_quantize(gu, out_map)
     assert np.array_equal(host_u16(sa2)[:, rows], sa_ref)
     assert np.array_equal(act_rows(host(A2), out_map, M, rows), A_ref)
+
+
+def test_fused_swiglu_few_tokens_across_workspace_growth():
+    """The few-token fused path writes its fp16 gate/up output to a buffer kept
+    per stream beside the split-K buffers.  Split GEMMs that grow those buffers
+    in between (8 and then 32 split tiles) must leave the fused path exact, and
+    the split GEMMs must match the oracle."""
+    K = 1024
+    steps = [("fused", 32, 1024), ("split", 512, 1024), ("fused", 40, 2048),
+             ("split", 1024, 2048), ("fused", 24, 1024)]
+    for kind, M, N in steps:
+        print(f"workspace growth: {kind} M={M} N={N} K={K}", flush=True)
+        NG = K // 128
+        prec = synth.prec_map(NG, max(1, NG // 8))
+        X16 = synth.activations(M + N, M, K, prec)
+        W16 = synth.weights(M + N, N, K)
+        A, sa = comet.quantize_act(dev_u16(X16), prec)
+        Wp, sw = comet.pack_w4(dev_u16(W16))
+        out = comet.w4ax_gemm(A, prec, sa, Wp, sw, M, N, K)
+        if kind == "split":
+            rows = np.array([0, 1, 255, 256, M - 1])
+            qa, osa = oracle.quantize_act(X16[rows], prec)
+            qw, osw = oracle.quantize_weight(W16)
+            ref = oracle.dequant_gemm(qa, osa, qw, osw)
+            assert_out_close(host_u16(out).view(np.float16)[rows], ref, f"split {M}x{N}x{K}")
+        else:
+            out_map = synth.prec_map(N // 2 // 128, 1, "random", seed=N)
+            A2, sa2 = comet.w4ax_gemm_swiglu_quant(A, prec, sa, Wp, sw, M, N, K, out_map)
+            A_ref, sa_ref = oracle.swiglu_quantize(host_u16(out), out_map)
+            assert np.array_equal(host_u16(sa2), sa_ref)
+            assert np.array_equal(host(A2), A_ref)
