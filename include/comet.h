@@ -182,7 +182,8 @@ COMET_API comet_status_t comet_kv4_dequantize(const uint8_t* codes, const uint16
  * w_scales[g][n] * sum_{c<G} qa[m][gG+c] * qw[n][gG+c] ).  The per-block sums
  * are exact; the sum over blocks is fp32 in an unspecified order, rounded once
  * to fp16 (nearest even).  Output is deterministic for a given build, device,
- * shape and map.  N must be a multiple of 16. */
+ * shape and map.  N must be a multiple of 16; M at most 2,097,120 (larger M:
+ * COMET_ERR_UNSUPPORTED). */
 COMET_API comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* group_prec_map,
                                const uint16_t* a_scales, const uint8_t* W_packed,
                                const uint16_t* w_scales, uint16_t* out, int M, int N, int K,

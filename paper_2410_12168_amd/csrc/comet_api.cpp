@@ -108,6 +108,9 @@ comet_status_t gemm_common(const uint8_t* A, const uint8_t* prec, const uint16_t
                                   int K, int G, comet::BlockMap* map) {
   if (!A || !sa || !W || !sw || !out) return fail(COMET_ERR_INVALID_ARG, "null pointer");
   if (M < 1 || N < 1) return fail(COMET_ERR_INVALID_ARG, "M=%d, N=%d must be >= 1", M, N);
+  // the kernels address rows within one activation block with 32-bit offsets
+  if (M > kMaxQuantRows)
+    return fail(COMET_ERR_UNSUPPORTED, "M=%d exceeds %d rows per call", M, kMaxQuantRows);
   if (N % 16) return fail(COMET_ERR_INVALID_ARG, "N=%d must be a multiple of 16", N);
   comet_status_t st = check_kg(K, G);
   if (st) return st;
@@ -549,8 +552,6 @@ comet_status_t comet_w4ax_gemm_swiglu_quant(const uint8_t* A_packed, const uint8
   comet_status_t st = gemm_common(A_packed, prec, a_scales, W_packed, w_scales, out_A_packed, M,
                                   N, K, G, &map);
   if (st) return st;
-  if (M > kMaxQuantRows)
-    return fail(COMET_ERR_UNSUPPORTED, "M=%d exceeds %d rows per call", M, kMaxQuantRows);
   SwigluOut so{out_A_packed, out_a_scales, {}};
   if ((st = make_map(out_prec, N / 2 / G, &so.map))) return st;
   return run_gemm(A_packed, prec, a_scales, W_packed, w_scales, nullptr, nullptr, M, N, K, map, 0,

@@ -51,7 +51,7 @@ def gemm(prec=(4, 8), M=16, N=32, K=256, G=128, A=FAKE, out=FAKE):
 @pytest.mark.parametrize("kw,status", [
     (dict(M=0), 1), (dict(N=0), 1), (dict(N=24), 1), (dict(K=200), 1), (dict(K=64), 1),
     (dict(G=64, K=256), 2), (dict(prec=(4, 5)), 1), (dict(A=0), 1), (dict(out=FAKE + 8), 1),
-    (dict(K=65536 + 128, prec=(4,) * 513), 2),
+    (dict(K=65536 + 128, prec=(4,) * 513), 2), (dict(M=65535 * 32 + 1), 2),
 ])
 def test_gemm_argument_errors(kw, status):
     assert gemm(**kw) == status
