@@ -99,6 +99,20 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _tensor(t, dtype: str, name: str):
+    """A convenience wrapper's tensor argument.  The kernels read plain
+    row-major device memory, so a view with strides, another dtype or a host
+    tensor would be misread; they are rejected here instead."""
+    import torch
+
+    want = getattr(torch, dtype)
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != want or not t.is_contiguous():
+        got = (f"{t.dtype} on {t.device}{'' if t.is_contiguous() else ', strided'}"
+               if isinstance(t, torch.Tensor) else type(t).__name__)
+        raise ValueError(f"{name}: need a contiguous {dtype} CUDA tensor, got {got}")
+    return t
+
+
 def _map(prec) -> np.ndarray:
     m = np.ascontiguousarray(np.asarray(prec, dtype=np.uint8))
     return m
@@ -228,6 +242,9 @@ def quantize_act(X, group_prec_map, perm=None, stream=None):
     perm: optional int32 [K] CUDA tensor (channel permutation)."""
     import torch
 
+    _tensor(X, "float16", "X")
+    if perm is not None:
+        _tensor(perm, "int32", "perm")
     M, K = X.shape
     nbytes = comet_act_packed_bytes(group_prec_map, M, K)
     if nbytes == 0:
@@ -243,6 +260,9 @@ def pack_w4(W, perm=None, stream=None):
     perm: optional int32 [K] CUDA tensor (the activations' channel permutation)."""
     import torch
 
+    _tensor(W, "float16", "W")
+    if perm is not None:
+        _tensor(perm, "int32", "perm")
     N, K = W.shape
     Wp = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
     sw = torch.empty((K // G, N), dtype=torch.float16, device=W.device)
@@ -254,9 +274,11 @@ def channel_absmax(X, absmax=None, stream=None):
     """Running per-channel max |X| (float32 [K] CUDA tensor), accumulated into absmax."""
     import torch
 
+    _tensor(X, "float16", "X")
     M, K = X.shape
     if absmax is None:
         absmax = torch.zeros(K, dtype=torch.float32, device=X.device)
+    _tensor(absmax, "float32", "absmax")
     comet_channel_absmax(X, absmax, M, K, stream)
     return absmax
 
@@ -277,6 +299,7 @@ def kv4_quantize(X, G: int = 128, stream=None):
     """X: float16 [T][C] CUDA tensor -> (codes uint8 [T][C/2], params float16 [T][C/G][2])."""
     import torch
 
+    _tensor(X, "float16", "X")
     T, C = X.shape
     codes = torch.empty((T, C // 2), dtype=torch.uint8, device=X.device)
     params = torch.empty((T, C // G, 2), dtype=torch.float16, device=X.device)
@@ -287,18 +310,29 @@ def kv4_quantize(X, G: int = 128, stream=None):
 def kv4_dequantize(codes, params, G: int = 128, stream=None):
     import torch
 
+    _tensor(codes, "uint8", "codes")
+    _tensor(params, "float16", "params")
     T, C = codes.shape[0], codes.shape[1] * 2
     out = torch.empty((T, C), dtype=torch.float16, device=codes.device)
     comet_kv4_dequantize(codes, params, out, T, C, G, stream)
     return out
 
 
+def _gemm_operands(A_packed, a_scales, W_packed, w_scales):
+    _tensor(A_packed, "uint8", "A_packed")
+    _tensor(a_scales, "float16", "a_scales")
+    _tensor(W_packed, "uint8", "W_packed")
+    _tensor(w_scales, "float16", "w_scales")
+
+
 def w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int, N: int, K: int,
               out=None, stream=None):
     import torch
 
+    _gemm_operands(A_packed, a_scales, W_packed, w_scales)
     if out is None:
         out = torch.empty((M, N), dtype=torch.float16, device=A_packed.device)
+    _tensor(out, "float16", "out")
     comet_w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, out, M, N, K, G,
                     stream)
     return out
@@ -310,6 +344,7 @@ def w4ax_gemm_swiglu_quant(A_packed, group_prec_map, a_scales, W_packed, w_scale
     Returns (out_A_packed uint8, out_a_scales float16 [I/G][M]), I = N / 2."""
     import torch
 
+    _gemm_operands(A_packed, a_scales, W_packed, w_scales)
     I = N // 2
     nbytes = comet_act_packed_bytes(out_prec_map, M, I)
     if nbytes == 0:
@@ -325,6 +360,7 @@ def swiglu_quantize(gu, out_prec_map, stream=None):
     """gu: float16 [M][2I] CUDA tensor (256-wide gate/up groups) -> (A_packed, a_scales)."""
     import torch
 
+    _tensor(gu, "float16", "gu")
     M, N = gu.shape
     I = N // 2
     nbytes = comet_act_packed_bytes(out_prec_map, M, I)
@@ -340,6 +376,7 @@ def w4ax_gemm_acc(A_packed, group_prec_map, a_scales, W_packed, w_scales, M: int
                   m0: int, m1: int, n0: int, n1: int, stream=None):
     import torch
 
+    _gemm_operands(A_packed, a_scales, W_packed, w_scales)
     acc = torch.empty((m1 - m0, n1 - n0, K // G), dtype=torch.int32, device=A_packed.device)
     comet_w4ax_gemm_acc(A_packed, group_prec_map, a_scales, W_packed, w_scales, acc, M, N, K, G,
                         m0, m1, n0, n1, stream)

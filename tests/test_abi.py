@@ -108,3 +108,18 @@ def test_unsupported_architecture_is_reported():
 def test_status_strings():
     assert comet.comet_status_str(0) == "COMET_OK"
     assert comet.comet_status_str(2) == "COMET_ERR_UNSUPPORTED"
+
+
+def test_wrappers_reject_host_tensors():
+    # checked before any library call: the kernels read plain device memory
+    import torch
+
+    X = torch.zeros((4, 256), dtype=torch.float16)
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        comet.quantize_act(X, [4, 8])
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        comet.pack_w4(X)
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        comet.kv4_quantize(X)
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        comet.w4ax_gemm(X, [4, 8], X, X, X, 4, 16, 256)

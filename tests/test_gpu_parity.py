@@ -222,3 +222,15 @@ def test_llama3_70b_decode_128_row_tiles_sampled_rows(M):
     qw, sw = oracle.quantize_weight(r["W16"])
     ref = oracle.dequant_gemm(qa, sa, qw, sw)
     assert_out_close(host_u16(r["out"]).view(np.float16)[rows], ref, f"decode M={M}")
+
+
+def test_wrappers_reject_strided_and_mistyped_tensors():
+    X = torch.zeros((256, 128), dtype=torch.float16, device=DEV)
+    with pytest.raises(ValueError, match="strided"):
+        comet.quantize_act(X.t(), [4, 8])
+    with pytest.raises(ValueError, match="float32"):
+        comet.pack_w4(X.float())
+    A, sa = comet.quantize_act(X[:, :128].contiguous(), [4])
+    Wp, sw = comet.pack_w4(X[:16].contiguous())
+    with pytest.raises(ValueError, match="a_scales"):
+        comet.w4ax_gemm(A, [4], sa.view(torch.int16), Wp, sw, 256, 16, 128)
