@@ -123,3 +123,18 @@ def test_wrappers_reject_host_tensors():
         comet.kv4_quantize(X)
     with pytest.raises(ValueError, match="CUDA tensor"):
         comet.w4ax_gemm(X, [4, 8], X, X, X, 4, 16, 256)
+
+
+def test_missing_library_raises(monkeypatch, tmp_path):
+    # no fallback: without libcomet.so and with a failing build, the first
+    # call raises the build's error
+    import paper_2410_12168_amd.build as build_mod
+
+    def failing_build(*a, **k):
+        raise RuntimeError("hipcc failed (forced)")
+
+    monkeypatch.setattr(comet, "_lib", None)
+    monkeypatch.setattr(comet, "LIB_PATH", str(tmp_path / "libcomet.so"))
+    monkeypatch.setattr(build_mod, "build", failing_build)
+    with pytest.raises(RuntimeError, match="forced"):
+        comet.comet_act_packed_bytes([4], 1, 128)
