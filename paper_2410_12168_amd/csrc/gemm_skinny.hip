@@ -38,7 +38,8 @@ constexpr int kWaves = 4;  // waves per workgroup; the split-K slot count divide
 // One K-block's activation fragments and scales, loaded one step ahead.  Both
 // 16-byte halves are always loaded (for a 4-bit block the second repeats the
 // first), so every step issues the same loads and the compiler's waits stay
-// partial.
+// partial.  With at most 8 rows one load per lane suffices (load_a's HALF
+// form, which leaves a[r][1] unused).
 template <int R>
 struct AStep {
   u32x4 a[R][2];
@@ -70,12 +71,24 @@ __device__ __forceinline__ int aoff_of(const GemmArgs& p, int g) {
 
 // Activation fragments (rows 16 r + lane % 16, 32 codes of quarter lane / 16)
 // and scales of K-block g, whose block starts at aoff * M * 64 bytes.
-template <int R>
+template <int R, bool HALF = false>
 __device__ __forceinline__ void load_a(const GemmArgs& p, int g, int aoff, int col, AStep<R>& s) {
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, q4 = lane >> 4;
   const uint32_t b8 = is8(p, g) ? 1u : 0u;
   const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)aoff;
+  if constexpr (HALF) {
+    // M <= 8: rows 8..15 of the fragment are padding.  Lane r of each
+    // 16-lane row loads row r & 7: its (first) 16 bytes for r < 8, and for an
+    // 8-bit block the second 16 bytes of the same 32-byte chunk for r >= 8.
+    // compute_step moves the second halves down by eight lanes.
+    const uint32_t row = (uint32_t)min(r16 & 7, p.M - 1);
+    const uint32_t second = ((uint32_t)r16 >> 3) & b8;
+    s.a[0][0] = *reinterpret_cast<const u32x4*>(A + (row << (6 + b8)) + ((uint32_t)q4 << (4 + b8)) +
+                                               (second << 4));
+    (void)col;
+    return;
+  }
   #pragma unroll
   for (int r = 0; r < R; ++r) {
     const uint32_t row = (uint32_t)min(16 * r + r16, p.M - 1);
@@ -113,7 +126,7 @@ __device__ __forceinline__ void load_w(const GemmArgs& p, int gb, int glast, int
   }
 }
 
-template <int R, bool DIAG>
+template <int R, bool DIAG, bool HALF = false>
 __device__ __forceinline__ void compute_step(const GemmArgs& p, const u32x4& wraw, int i, int g,
                                              bool b8, int n0, const AStep<R>& s,
                                              const SBatch<R>& sc, f32x4 (&C)[R]) {
@@ -129,12 +142,19 @@ __device__ __forceinline__ void compute_step(const GemmArgs& p, const u32x4& wra
     f32x4 y;
     if (b8) {
       i32x8 al, ah;
+      u32x4 x1 = s.a[r][1];
+      if constexpr (HALF) {
+        // second 16 bytes from the lane eight above, in the same 16-lane row
+        #pragma unroll
+        for (int k = 0; k < 4; ++k)
+          x1[k] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)s.a[r][0][k], 0x128, 0xF, 0xF, false);
+      }
       #pragma unroll
       for (int k = 0; k < 4; ++k) {
         al[k] = (int)lo8(s.a[r][0][k]);
-        al[4 + k] = (int)lo8(s.a[r][1][k]);
+        al[4 + k] = (int)lo8(x1[k]);
         ah[k] = (int)hi8(s.a[r][0][k]);
-        ah[4 + k] = (int)hi8(s.a[r][1][k]);
+        ah[4 + k] = (int)hi8(x1[k]);
       }
       const f32x4 yh = mfma_fp8(ah, wf, f32x4{0.f, 0.f, 0.f, 0.f});
       y = mfma_fp8(al, wf, yh * 8.0f);  // exact: integers below 2^24 units
@@ -184,7 +204,7 @@ __device__ __forceinline__ void issue_point() {
 // `wc`, while the next batch's weights load into `wn`.  The activation step
 // of K-block gb is in `x` on entry; `x` and `y` alternate, and the step of
 // K-block gb + 4 is in `x` on exit.
-template <int R, bool DIAG>
+template <int R, bool DIAG, bool HALF>
 __device__ __forceinline__ void batch(const GemmArgs& p, int gb, int g1, int n0, int col,
                                       int& aoff, const u32x4 (&wc)[4], u32x4 (&wn)[4],
                                       const SBatch<R>& sc, SBatch<R>& sn, AStep<R>& x,
@@ -201,9 +221,9 @@ __device__ __forceinline__ void batch(const GemmArgs& p, int gb, int g1, int n0,
     const int an = g + 1 < NG ? aoff + 1 + (b8 ? 1 : 0) : aoff;
     AStep<R>& cur = (i & 1) ? y : x;
     AStep<R>& nxt = (i & 1) ? x : y;
-    load_a<R>(p, gn, an, col, nxt);
+    load_a<R, HALF>(p, gn, an, col, nxt);
     issue_point();
-    if (g < g1) compute_step<R, DIAG>(p, wc[i], i, g, b8, n0, cur, sc, C);
+    if (g < g1) compute_step<R, DIAG, HALF>(p, wc[i], i, g, b8, n0, cur, sc, C);
     aoff = an;
   }
 }
@@ -214,7 +234,7 @@ __device__ __forceinline__ void batch(const GemmArgs& p, int gb, int g1, int n0,
 // slot order.  (A cross-workgroup reduction would need device-scope fences,
 // and on this multi-XCD part each one writes back and invalidates the XCD's
 // L2: measured ~12x slower for a 70B-sized weight stream.)
-template <int R, bool DIAG>
+template <int R, bool DIAG, bool HALF>
 __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
   __shared__ f32x4 red[kWaves][R][64];
   const int lane = threadIdx.x & 63;
@@ -240,12 +260,12 @@ __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(GemmArgs p) {
     int aoff = aoff_of(p, g0);
     load_w(p, g0, g1 - 1, n0, wa);
     load_scales<R>(p, g0, n0, sa_);
-    load_a<R>(p, g0, aoff, col, x);
+    load_a<R, HALF>(p, g0, aoff, col, x);
     for (int gb = g0;;) {
-      batch<R, DIAG>(p, gb, g1, n0, col, aoff, wa, wb, sa_, sb_, x, y, C);
+      batch<R, DIAG, HALF>(p, gb, g1, n0, col, aoff, wa, wb, sa_, sb_, x, y, C);
       gb += kD;
       if (gb >= g1) break;
-      batch<R, DIAG>(p, gb, g1, n0, col, aoff, wb, wa, sb_, sa_, x, y, C);
+      batch<R, DIAG, HALF>(p, gb, g1, n0, col, aoff, wb, wa, sb_, sa_, x, y, C);
       gb += kD;
       if (gb >= g1) break;
     }
@@ -277,10 +297,18 @@ template <int R>
 hipError_t launch_r(const GemmArgs& a, bool diag, hipStream_t stream) {
   const int per_wg = kWaves / a.splits;
   const int blocks = (a.N / 16 + per_wg - 1) / per_wg;
-  if (diag)
-    hipLaunchKernelGGL((skinny_kernel<R, true>), dim3(blocks), dim3(kWaves * 64), 0, stream, a);
-  else
-    hipLaunchKernelGGL((skinny_kernel<R, false>), dim3(blocks), dim3(kWaves * 64), 0, stream, a);
+  const bool half = R == 1 && a.M <= 8;
+  if (diag) {
+    if (half)
+      hipLaunchKernelGGL((skinny_kernel<1, true, true>), dim3(blocks), dim3(kWaves * 64), 0, stream, a);
+    else
+      hipLaunchKernelGGL((skinny_kernel<R, true, false>), dim3(blocks), dim3(kWaves * 64), 0, stream, a);
+  } else {
+    if (half)
+      hipLaunchKernelGGL((skinny_kernel<1, false, true>), dim3(blocks), dim3(kWaves * 64), 0, stream, a);
+    else
+      hipLaunchKernelGGL((skinny_kernel<R, false, false>), dim3(blocks), dim3(kWaves * 64), 0, stream, a);
+  }
   return hipGetLastError();
 }
 
