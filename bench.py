@@ -61,7 +61,16 @@ KERNEL_SOURCES = {
     "kv4": ["kv4.hip"],
 }
 SKINNY_MAX_M = 48  # the library runs the few-token kernel up to this M,
+SKINNY_WIDE_M = 32  # except above this M when 256-column tiles cover 3/4 of the CUs,
 MID_MAX_M = 128    # and the 128-row-tile kernel up to this one
+
+
+def gemm_kind(M: int, N: int, cus: int) -> str:
+    """Which GEMM kernel the library runs for this shape (the same rule)."""
+    wide = 4 * ((N + 255) // 256) >= 3 * cus
+    if M <= SKINNY_MAX_M and not (M > SKINNY_WIDE_M and wide):
+        return "skinny"
+    return "mid" if M <= MID_MAX_M else "tile"
 
 
 def kernel_sha(kind: str) -> str:
@@ -266,7 +275,7 @@ def main():
     # the dominant kernel launch: the GEMM of the layer with the most work
     d = int(np.argmax(ops))
     D = layers[d]
-    kind = "skinny" if M <= SKINNY_MAX_M else ("mid" if M <= MID_MAX_M else "tile")
+    kind = gemm_kind(M, D["N"], torch.cuda.get_device_properties(0).multi_processor_count)
     if hbm_bound:
         achieved = float(gbytes[d] / (g_ms[d] * 1e-3) / 1e9)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,

@@ -328,7 +328,9 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
     g_attr_set[dev] = true;
   }
   const bool diag = acc != nullptr;
-  const bool skinny = M <= comet::kSkinnyMaxM;
+  const int col_tiles = (N + comet::kTileN - 1) / comet::kTileN;
+  const bool skinny =
+      M <= comet::kSkinnyMaxM && !(M > comet::kSkinnyWideM && 4 * col_tiles >= 3 * info.cus);
   const DevicePlan* plan;
   // the diagnostic form of the tile kernel runs whole tiles (no split partials)
   if ((st = get_plan(dev, info.cus, M, N, K, prec, map, diag ? std::string("dp") : sched_mode(),

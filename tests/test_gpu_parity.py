@@ -210,14 +210,15 @@ def test_llama3_70b_decode_full_size(M):
     assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"decode M={M}")
 
 
-@pytest.mark.parametrize("M", [96, 128])
+@pytest.mark.parametrize("M", [40, 96, 128])
 def test_llama3_70b_decode_128_row_tiles_sampled_rows(M):
-    # LLaMA-3-70B gate_up with 128-row tiles; a sample of rows on both halves
-    # of the tile checked against the oracle
+    # LLaMA-3-70B gate_up with 128-row tiles (at M = 40 too: its 224 column
+    # tiles are wide enough to take it from the few-token kernel); a sample of
+    # rows on both halves of the tile checked against the oracle
     K, N = synth.LLAMA3_70B["gate_up"]
     prec = synth.prec_map(K // 128, K // 128 // 16)
     r = run_path(M, N, K, prec, seed=M)
-    rows = np.array([0, 1, 63, 64, M - 1])
+    rows = np.unique(np.clip([0, 1, 63, 64, M - 1], 0, M - 1))
     qa, sa = oracle.quantize_act(r["X16"][rows], prec)
     qw, sw = oracle.quantize_weight(r["W16"])
     ref = oracle.dequant_gemm(qa, sa, qw, sw)
