@@ -37,6 +37,10 @@ comet_status_t ok() {
   return COMET_OK;
 }
 
+// Above this many rows the 128-row tile kernel takes over from the few-token
+// kernel when its 256-column tiles cover at least 3/4 of the CUs (wide N).
+constexpr int kSkinnyWideM = 32;
+
 // The activation quantizer's grid has one row of workgroups per 32 tokens.
 constexpr int kMaxQuantRows = 65535 * 32;
 
@@ -330,7 +334,7 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   const bool diag = acc != nullptr;
   const int col_tiles = (N + comet::kTileN - 1) / comet::kTileN;
   const bool skinny =
-      M <= comet::kSkinnyMaxM && !(M > comet::kSkinnyWideM && 4 * col_tiles >= 3 * info.cus);
+      M <= comet::kSkinnyMaxM && !(M > kSkinnyWideM && 4 * col_tiles >= 3 * info.cus);
   const DevicePlan* plan;
   // the diagnostic form of the tile kernel runs whole tiles (no split partials)
   if ((st = get_plan(dev, info.cus, M, N, K, prec, map, diag ? std::string("dp") : sched_mode(),

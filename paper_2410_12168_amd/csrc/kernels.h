@@ -89,9 +89,6 @@ hipError_t launch_swiglu_quantize(const uint16_t* GU, uint8_t* A, uint16_t* sa, 
                                   const BlockMap& map, hipStream_t stream);
 // Few-token kernel (M <= kSkinnyMaxM): one wave per (16 columns, split-K slot).
 constexpr int kSkinnyMaxM = 48;
-// Above this many rows the 128-row tile kernel takes over from the few-token
-// kernel when its 256-column tiles cover at least 3/4 of the CUs (wide N).
-constexpr int kSkinnyWideM = 32;
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
 // Split-K slots (1, 2 or 4) for the few-token kernel: spread the (N/16 x
 // slots) waves evenly over the device's SIMDs, keeping at least 4 K-blocks per
