@@ -57,20 +57,15 @@ CSRC = os.path.join(ROOT, "paper_2410_12168_amd", "csrc")
 KERNEL_SOURCES = {
     "tile": ["gemm.hip", "operand.h", "kernels.h"],
     "skinny": ["gemm_skinny.hip", "operand.h", "kernels.h"],
+    "skinny_shared": ["gemm_skinny.hip", "operand.h", "kernels.h"],
     "mid": ["gemm.hip", "operand.h", "kernels.h"],
     "kv4": ["kv4.hip"],
 }
-SKINNY_MAX_M = 48  # the library runs the few-token kernel up to this M,
-SKINNY_WIDE_M = 32  # except above this M when 256-column tiles cover 3/4 of the CUs,
-MID_MAX_M = 128    # and the 128-row-tile kernel up to this one
+def gemm_kind(M: int, N: int, K: int, cus: int) -> str:
+    """Which GEMM kernel the library runs for this shape (asked of the library)."""
+    import paper_2410_12168_amd as comet
 
-
-def gemm_kind(M: int, N: int, cus: int) -> str:
-    """Which GEMM kernel the library runs for this shape (the same rule)."""
-    wide = 4 * ((N + 255) // 256) >= 3 * cus
-    if M <= SKINNY_MAX_M and not (M > SKINNY_WIDE_M and wide):
-        return "skinny"
-    return "mid" if M <= MID_MAX_M else "tile"
+    return comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, cus)]
 
 
 def kernel_sha(kind: str) -> str:
@@ -132,6 +127,10 @@ def parse():
                          "quantization (weights packed with the same permutation)")
     ap.add_argument("--cpu-rows", type=int, default=512,
                     help="token rows per layer in the CPU-oracle sample (0: skip)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="llama3-70b-prefill: skip the other configurations (small case, "
+                         "LLaMA-3-8B layers, load-balance sweep with the schedule ablation, "
+                         "decode sweep) that the default run reports beside the headline")
     return ap.parse_args()
 
 
@@ -275,7 +274,7 @@ def main():
     # the dominant kernel launch: the GEMM of the layer with the most work
     d = int(np.argmax(ops))
     D = layers[d]
-    kind = gemm_kind(M, D["N"], torch.cuda.get_device_properties(0).multi_processor_count)
+    kind = gemm_kind(M, D["N"], D["K"], torch.cuda.get_device_properties(0).multi_processor_count)
     if hbm_bound:
         achieved = float(gbytes[d] / (g_ms[d] * 1e-3) / 1e9)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
@@ -327,10 +326,25 @@ def main():
         torch.cuda.synchronize()
         record["copy_mib"] = args.copy_mib
 
+    if args.workload == "llama3-70b-prefill" and not args.no_extras and not args.m and \
+            not args.layers and not args.perm:
+        record["configs"] = bench_extras(args, dev, layers)
+
     if args.cpu_rows > 0:
         record["cpu_baseline"] = cpu_baseline(layers, args.cpu_rows)
 
     print(json.dumps(record), flush=True)
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(layers, rows_per_layer: int) -> dict:
@@ -363,13 +377,247 @@ def cpu_baseline(layers, rows_per_layer: int) -> dict:
         mx, norm = out_errors(y, ref)
         worst = max(worst, mx)
         worst_norm = max(worst_norm, norm)
+    # one thread on the small case (16 x 1024 x 1024, block 3 of 8 in 8 bits):
+    # a per-core figure, median of three runs
+    import synth
+
+    prec0 = synth.prec_map(8, 1)
+    X0, W0 = synth.activations(0, 16, 1024, prec0), synth.weights(0, 1024, 1024)
+    qw0, sw0 = oracle.quantize_weight(W0, nthreads=1)
+    t1 = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        qa0, sa0 = oracle.quantize_act(X0, prec0, nthreads=1)
+        oracle.dequant_gemm(qa0, sa0, qw0, sw0, nthreads=1)
+        t1.append(time.perf_counter() - t0)
+    t1 = float(np.median(t1))
     return {
         "value": round(ops / t_total / 1e12, 5), "unit": "TOPS", "cores": threads,
-        "kind": "oracle", "seconds": round(t_total, 2),
+        "kind": "oracle", "seconds": round(t_total, 2), "cpu_model": cpu_model(),
+        "rows_per_layer": int(min(rows_per_layer, layers[0]["M"])),
         "sample": ", ".join(f"{L['name']}: first {min(rows_per_layer, L['M'])} of {L['M']} token rows"
-                            for L in layers) + " (quantize + fp64-dequant GEMM)",
+                            for L in layers) + " (quantize + fp64-dequant GEMM); value = "
+                  "2*rows*N*K summed over the sample / oracle seconds",
+        "single_thread_small_case": {
+            "workload": "M=16, K=N=1024, G=128, block 3 of 8 in 8 bits (quantize + GEMM), "
+                        "median of 3", "seconds": round(t1, 5), "cores": 1,
+            "value": round(2.0 * 16 * 1024 * 1024 / t1 / 1e12, 6), "unit": "TOPS"},
         "parity_max_rel": worst, "parity_norm_rel": worst_norm, "parity_ok": worst <= 2e-3,
     }
+
+
+def _to_dev(a16, dev):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a16).view(np.int16)).to(dev).view(torch.float16)
+
+
+def _ms_per_call(fn, n: int, warm: int = 2) -> float:
+    """Average time of `fn(i)` over n back-to-back calls, from HIP events
+    around the batch on the current stream (the one the library launches on)."""
+    import torch
+
+    for i in range(warm):
+        fn(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(n):
+        fn(i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / n
+
+
+def _rows_err(out, X16, prec, qw, sw, rows) -> float:
+    """Max elementwise error (tests/parity.py rule) of the fp16 output rows
+    against the CPU oracle."""
+    import torch
+
+    import oracle
+    from parity import out_errors
+
+    qa, sa = oracle.quantize_act(X16[rows], prec)
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    idx = torch.from_numpy(np.asarray(rows)).to(out.device)
+    y = out[idx].view(torch.int16).cpu().numpy().view(np.float16)
+    return out_errors(y, ref)[0]
+
+
+def _gemm_bytes(M, N, K, n8):
+    k8 = 128 * n8
+    return N * K / 2 + 2 * N * (K // 128) + M * ((K - k8) / 2 + k8) + 2 * M * (K // 128) + 2 * M * N
+
+
+def bench_extras(args, dev, main_layers) -> dict:
+    """The other benchmark configurations, measured in the same run beside the
+    headline (each GEMM timed over back-to-back calls with HIP events; fp16
+    outputs of sampled rows checked against the CPU oracle):
+      small: M = 16, K = N = 1024, block 3 of 8 in 8 bits (launch-bound);
+      llama3_8b: the four LLaMA-3-8B layers at M = 2048;
+      load_balance: LLaMA-3-70B down (M = 4096, K = 28672, N = 8192) with 0,
+        1/16, 1/4 and 1/2 of the blocks 8-bit, contiguous or random;
+      ablation: the schedule modes natural (map order, whole tiles), dp
+        (precision-batched order, whole tiles) and cost (the default: plus a
+        cost-balanced split of the last wave of tiles) on the load-balance
+        points and on the 70B qkv layer;
+      decode: LLaMA-3-70B gate_up at M = 1, 8, 32, 128 with six rotated weight
+        copies, so every call streams its weights from HBM."""
+    import torch
+
+    import oracle
+    import paper_2410_12168_amd as comet
+    import synth
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    res = {}
+    seed = args.seed
+
+    def mode(m):
+        if m is None:
+            os.environ.pop("COMET_SCHED", None)
+        else:
+            os.environ["COMET_SCHED"] = m
+
+    # small case
+    M, K, N = 16, 1024, 1024
+    prec = synth.prec_map(K // 128, 1)
+    X16, W16 = synth.activations(seed, M, K, prec), synth.weights(seed, N, K)
+    X, Wd = _to_dev(X16, dev), _to_dev(W16, dev)
+    Wp, sw = comet.pack_w4(Wd)
+    A, sa = comet.quantize_act(X, prec)
+    out = torch.empty((M, N), dtype=torch.float16, device=dev)
+
+    def small_both(i):
+        comet.comet_fmpq_quantize_act(X, prec, A, sa, M, K)
+        comet.comet_w4ax_gemm(A, prec, sa, Wp, sw, out, M, N, K)
+
+    t_both = _ms_per_call(small_both, 200)
+    t_gemm = _ms_per_call(lambda i: comet.comet_w4ax_gemm(A, prec, sa, Wp, sw, out, M, N, K), 200)
+    qw, osw = oracle.quantize_weight(W16)
+    res["small"] = {"workload": "M=16, K=N=1024, G=128, block 3 of 8 in 8 bits",
+                    "kernel": comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, cus)],
+                    "quant_plus_gemm_us": round(t_both * 1e3, 2),
+                    "gemm_us": round(t_gemm * 1e3, 2),
+                    "parity_max_rel": _rows_err(out, X16, prec, qw, osw, np.arange(M))}
+
+    # LLaMA-3-8B layers at M = 2048
+    M = 2048
+    layers8 = {}
+    for name, (K, N) in synth.LLAMA3_8B.items():
+        NG = K // 128
+        prec = synth.prec_map(NG, NG // 16)
+        X16, W16 = synth.activations(seed, M, K, prec), synth.weights(seed, N, K)
+        X, Wd = _to_dev(X16, dev), _to_dev(W16, dev)
+        Wp, sw = comet.pack_w4(Wd)
+        del Wd
+        A, sa = comet.quantize_act(X, prec)
+        out = torch.empty((M, N), dtype=torch.float16, device=dev)
+        tq = _ms_per_call(lambda i: comet.comet_fmpq_quantize_act(X, prec, A, sa, M, K), 10)
+        tg = _ms_per_call(lambda i: comet.comet_w4ax_gemm(A, prec, sa, Wp, sw, out, M, N, K), 10)
+        ops = 2.0 * M * N * K
+        qw, osw = oracle.quantize_weight(W16)
+        rows = np.arange(0, M, 256) + 17  # one row in every 256-row tile
+        layers8[name] = {"K": K, "N": N, "gemm_us": round(tg * 1e3, 2),
+                         "gemm_frac_peak": round(ops / (tg * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+                         "quant_us": round(tq * 1e3, 2),
+                         "parity_max_rel": _rows_err(out, X16, prec, qw, osw, rows)}
+        del X, A, sa, out, Wp, sw
+    res["llama3_8b"] = {"M": M, "frac8": 1 / 16, "layers": layers8}
+
+    # load-balance sweep on the 70B down projection, with the schedule ablation
+    M, (K, N) = 4096, synth.LLAMA3_70B["down"]
+    NG = K // 128
+    W16 = synth.weights(seed, N, K)
+    Wd = _to_dev(W16, dev)
+    Wp, sw = comet.pack_w4(Wd)
+    del Wd
+    qw, osw = oracle.quantize_weight(W16)
+    out = torch.empty((M, N), dtype=torch.float16, device=dev)
+    ops = 2.0 * M * N * K
+    sweep, abl = {}, {}
+    for frac in (0.0, 1 / 16, 1 / 4, 1 / 2):
+        for place in ("contiguous", "random"):
+            if frac == 0.0 and place == "random":
+                continue  # no 8-bit blocks: the same map
+            n8 = int(round(NG * frac))
+            prec = synth.prec_map(NG, n8, place, seed=seed)
+            X16 = synth.activations(seed, M, K, prec)
+            X = _to_dev(X16, dev)
+            A, sa = comet.quantize_act(X, prec)
+            del X
+            key = f"f={frac:g},{place}"
+            t = {}
+            for m in ("natural", "dp", "cost"):
+                mode(m)
+                t[m] = _ms_per_call(
+                    lambda i: comet.comet_w4ax_gemm(A, prec, sa, Wp, sw, out, M, N, K), 5)
+            mode(None)
+            err = _rows_err(out, X16, prec, qw, osw, np.array([1, 1000, 2600, 4095]))
+            sweep[key] = {"n8": n8, "gemm_us": round(t["cost"] * 1e3, 2),
+                          "frac_peak": round(ops / (t["cost"] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+                          "parity_max_rel": err}
+            abl[f"down {key}"] = {m: round(v * 1e3, 2) for m, v in t.items()}
+            del A, sa
+    t0 = sweep["f=0,contiguous"]["gemm_us"]
+    for v in sweep.values():
+        v["t_over_t0"] = round(v["gemm_us"] / t0, 4)
+    res["load_balance"] = {"workload": "LLaMA-3-70B down, M=4096, K=28672, N=8192", "points": sweep}
+    del Wp, sw, out
+
+    # ablation on the 70B qkv layer of the headline step (640 tiles on 256 CUs)
+    for L in main_layers:
+        if L["name"] != "qkv":
+            continue
+        t = {}
+        for m in ("natural", "dp", "cost"):
+            mode(m)
+            t[m] = _ms_per_call(lambda i: comet.comet_w4ax_gemm(
+                L["A"], L["prec"], L["sa"], L["Wp"], L["sw"], L["out"], L["M"], L["N"], L["K"]), 10)
+        mode(None)
+        abl["qkv M=4096 f=1/16 contiguous"] = {m: round(v * 1e3, 2) for m, v in t.items()}
+    res["ablation_us"] = {"modes": "natural = map order, whole tiles; dp = precision-batched "
+                                   "order, whole tiles; cost = precision-batched + cost-balanced "
+                                   "split of the last wave (default)", "gemm_us": abl}
+
+    # decode sweep on the 70B gate_up with rotated weights
+    K, N = synth.LLAMA3_70B["gate_up"]
+    NG = K // 128
+    prec = synth.prec_map(NG, NG // 16)
+    W16 = synth.weights(seed, N, K)
+    Wd = _to_dev(W16, dev)
+    Wp, sw = comet.pack_w4(Wd)
+    del Wd
+    rot = 6
+    Wps = [Wp] + [Wp.clone() for _ in range(rot - 1)]
+    sws = [sw] + [sw.clone() for _ in range(rot - 1)]
+    qw, osw = oracle.quantize_weight(W16)
+    dec = {}
+    for M in (1, 8, 32, 128):
+        X16 = synth.activations(seed, M, K, prec)
+        A, sa = comet.quantize_act(_to_dev(X16, dev), prec)
+        out = torch.empty((M, N), dtype=torch.float16, device=dev)
+        t = _ms_per_call(lambda i: comet.comet_w4ax_gemm(A, prec, sa, Wps[i % rot], sws[i % rot],
+                                                         out, M, N, K), 60, warm=6)
+        nbytes = _gemm_bytes(M, N, K, NG // 16)
+        rows = np.arange(M) if M <= 32 else np.array([0, 1, 63, 64, 127])
+        dec[f"M={M}"] = {"kernel": comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, cus)],
+                         "gemm_us": round(t * 1e3, 2),
+                         "gbs": round(nbytes / (t * 1e-3) / 1e9, 1),
+                         "frac_hbm": round(nbytes / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                         "alg_bytes": int(nbytes),
+                         "parity_max_rel": _rows_err(out, X16, prec, qw, osw, rows)}
+    res["decode"] = {"workload": "LLaMA-3-70B gate_up, K=8192, N=57344, 1/16 of blocks 8-bit, "
+                                 f"{rot} rotated weight copies (back-to-back calls)", "points": dec}
+    del Wps, sws
+    torch.cuda.empty_cache()
+    worst = max([res["small"]["parity_max_rel"]] +
+                [v["parity_max_rel"] for v in layers8.values()] +
+                [v["parity_max_rel"] for v in sweep.values()] +
+                [v["parity_max_rel"] for v in dec.values()])
+    res["parity_max_rel"] = worst
+    res["parity_ok"] = worst <= 2e-3
+    return res
 
 
 def bench_mlp(args, wl, dev):

@@ -55,6 +55,19 @@
  *   - Faults inside kernels surface at the caller's next synchronisation.
  *   - Calls on different streams may run concurrently.  The GEMM's split-tile
  *     workspace is owned by the library, one per device and stream.
+ *   - The 128- and 256-row tile kernels run from a schedule (plan) that the
+ *     library builds on the host and uploads on the first call for each
+ *     (device, M, N, K, map, mode): that call allocates a few KB of device
+ *     memory and waits for the upload.  Plans stay cached until
+ *     comet_release_caches(), so the cache grows with every distinct shape;
+ *     the few-token kernels (small M) need no plan.
+ *   - The environment variable COMET_SCHED selects the schedule mode (Sec.
+ *     4.4, read at every call): "cost" (default: precision-batched K order,
+ *     data-parallel full waves of tiles, the last wave split by cost),
+ *     "dp" (precision-batched order, whole tiles only) or "natural" (the
+ *     map's own K order, whole tiles only: no tile remapping and no tile
+ *     decomposition).  Results do not depend on the mode beyond the fp32
+ *     summation order.
  */
 #ifndef COMET_H
 #define COMET_H
@@ -73,6 +86,14 @@ extern "C" {
 #endif
 
 typedef struct ihipStream_t* hipStream_t;
+
+/* GEMM kernels (comet_gemm_kernel). */
+typedef enum {
+  COMET_KERNEL_FEW_TOKEN = 0,         /* one wave per 16 columns and split-K slot */
+  COMET_KERNEL_FEW_TOKEN_SHARED = 1,  /* the same, activations shared through LDS */
+  COMET_KERNEL_MID = 2,               /* 128-row tiles */
+  COMET_KERNEL_TILE = 3               /* 256-row tiles */
+} comet_kernel_t;
 
 typedef enum {
   COMET_OK = 0,
@@ -251,6 +272,16 @@ COMET_API comet_status_t comet_schedule_query(int M, int N, int K, int G, const 
                                     int num_cus, int* units, int max_units, int* n_units,
                                     int* wg_begin, int max_wgs, int* n_wgs, int* order,
                                     int* tile_m, int* tile_n);
+
+/* Host-only: which GEMM kernel (comet_kernel_t) comet_w4ax_gemm runs for this
+ * shape on a device with `num_cus` compute units, or -1 for invalid
+ * arguments (comet_last_error() says why).  Nothing is launched. */
+COMET_API int comet_gemm_kernel(int M, int N, int K, int G, int num_cus);
+
+/* SHA-256 (64 hex digits) of the sources and build flags the library was
+ * built from; the same string follows "COMET_SOURCE_STAMP=" in the library
+ * file, so a loader can compare it with its source tree before loading. */
+COMET_API const char* comet_build_stamp(void);
 
 COMET_API const char* comet_status_str(comet_status_t status);
 

@@ -3,8 +3,16 @@
 Every HIP source is compiled for gfx950 only, with packed-fp32 instructions
 disabled, IEEE fp32 division and square root, fp32 denormals kept, and no
 floating-point contraction (fused multiply-adds are written explicitly).
+
+The library carries a stamp: the SHA-256 of its sources (csrc/, the public
+header) and of the compiler flags below, as the string
+``COMET_SOURCE_STAMP=<hex>`` in its data and from ``comet_build_stamp()``.
+``source_stamp()`` recomputes it from the tree, so a loader can tell a library
+built from other sources before it loads it.
 """
+import hashlib
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -31,12 +39,46 @@ DEVICE = ["-x", "hip", "--offload-arch=gfx950",
           "-munsafe-fp-atomics"]
 
 
-def _compile(src: str, verbose: bool) -> str:
+HEADER = os.path.join(os.path.dirname(HERE), "include", "comet.h")
+STAMP_RE = re.compile(rb"COMET_SOURCE_STAMP=([0-9a-f]{64})")
+
+
+def source_stamp() -> str:
+    """SHA-256 over every file under csrc/ (sorted by name), the public
+    header and the build flags."""
+    h = hashlib.sha256()
+    names = sorted(n for n in os.listdir(CSRC) if not n.startswith("."))
+    for name in names + [None]:
+        path = HEADER if name is None else os.path.join(CSRC, name)
+        h.update((name or "include/comet.h").encode() + b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    # flags without the include path, which depends on where the tree sits
+    flags = [f for f in COMMON if not f.startswith("-I")] + DEVICE
+    h.update(repr((SOURCES, PER_FILE, flags)).encode())
+    return h.hexdigest()
+
+
+def library_stamp(path: str = LIB):
+    """The stamp recorded in a built library file (read from its bytes,
+    without loading it), or None."""
+    try:
+        with open(path, "rb") as f:
+            m = STAMP_RE.search(f.read())
+    except OSError:
+        return None
+    return m.group(1).decode() if m else None
+
+
+def _compile(src: str, verbose: bool, stamp: str) -> str:
     path = os.path.join(CSRC, src)
     obj = os.path.join(OUT_DIR, src + ".o")
     cmd = [HIPCC] + COMMON
     if src.endswith(".hip"):
         cmd += DEVICE + PER_FILE.get(src, [])
+    if src == "comet_api.cpp":
+        cmd += [f'-DCOMET_SOURCE_STAMP="{stamp}"']
     cmd += ["-c", path, "-o", obj]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
@@ -54,13 +96,16 @@ def _compile(src: str, verbose: bool) -> str:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
+    stamp = source_stamp()
     with ThreadPoolExecutor(len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+        objs = list(ex.map(lambda s: _compile(s, verbose, stamp), SOURCES))
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
     subprocess.run(cmd, check=True)
+    if library_stamp(tmp) != stamp:
+        raise RuntimeError("built library does not carry the source stamp")
     os.replace(tmp, LIB)
     return LIB
 

@@ -18,7 +18,15 @@
 #include "kernels.h"
 #include "scheduler.h"
 
+#ifndef COMET_SOURCE_STAMP
+#define COMET_SOURCE_STAMP "unstamped"
+#endif
+
 namespace {
+
+// The build's source stamp, kept as one string so that a loader can find it
+// in the library file without loading it.
+const char kStamp[] = "COMET_SOURCE_STAMP=" COMET_SOURCE_STAMP;
 
 thread_local std::string g_last_error;
 
@@ -161,6 +169,20 @@ std::map<int, bool> g_attr_set;
 std::string sched_mode() {
   const char* m = std::getenv("COMET_SCHED");
   return (m && *m) ? std::string(m) : std::string("cost");
+}
+
+// Which GEMM kernel runs for this shape on `cus` compute units.  The
+// few-token kernels take M <= 48, except that above 32 rows the 128-row tile
+// kernel takes over when its 256-column tiles cover at least 3/4 of the CUs
+// (wide N); the 128-row tile kernel runs up to M = 128, the 256-row one above.
+int kernel_kind(int M, int N, int K, int cus) {
+  const int col_tiles = (N + comet::kTileN - 1) / comet::kTileN;
+  const bool wide = 4 * col_tiles >= 3 * cus;
+  if (M <= comet::kSkinnyMaxM && !(M > kSkinnyWideM && wide))
+    return comet::skinny_shared(M, comet::skinny_splits(N, K, cus))
+               ? COMET_KERNEL_FEW_TOKEN_SHARED
+               : COMET_KERNEL_FEW_TOKEN;
+  return comet::gemm_tile_m(M) == comet::kTileMSmall ? COMET_KERNEL_MID : COMET_KERNEL_TILE;
 }
 
 comet::PlanOptions plan_options(int M, int cus, const std::string& mode) {
@@ -332,18 +354,18 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
     g_attr_set[dev] = true;
   }
   const bool diag = acc != nullptr;
-  const int col_tiles = (N + comet::kTileN - 1) / comet::kTileN;
-  const bool skinny =
-      M <= comet::kSkinnyMaxM && !(M > kSkinnyWideM && 4 * col_tiles >= 3 * info.cus);
-  const DevicePlan* plan;
-  // the diagnostic form of the tile kernel runs whole tiles (no split partials)
-  if ((st = get_plan(dev, info.cus, M, N, K, prec, map, diag ? std::string("dp") : sched_mode(),
-                     stream, &plan)))
+  const int kind = kernel_kind(M, N, K, info.cus);
+  const bool skinny = kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED;
+  // the few-token kernels walk the K-blocks in natural order and need no plan
+  const DevicePlan* plan = nullptr;
+  if (!skinny &&
+      (st = get_plan(dev, info.cus, M, N, K, prec, map, sched_mode(), stream, &plan)))
     return st;
   comet::GemmArgs a{};
   a.splits = skinny ? comet::skinny_splits(N, K, info.cus) : 1;
   Workspace* ws = nullptr;
-  if (!skinny && plan->host.partial_slots > 0) {
+  // the diagnostic form writes every unit's blocks straight to acc: no partials
+  if (!skinny && !diag && plan->host.partial_slots > 0) {
     const size_t slots = (size_t)plan->host.partial_slots;
     if ((st = get_workspace(dev, stream, slots * plan->host.tile_m * plan->host.tile_n, slots,
                             &ws)))
@@ -357,16 +379,16 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   a.acc = acc;
   a.partials = ws ? ws->partials : nullptr;
   a.counters = ws ? ws->counters : nullptr;
-  a.units = plan->units;
-  a.wg_begin = plan->wg_begin;
-  a.order = plan->order;
-  a.split_index = plan->split_index;
-  a.n4 = 0;
-  for (int g = 0; g < K / comet::kG; ++g) a.n4 += prec[g] == 4;
+  if (plan) {
+    a.units = plan->units;
+    a.wg_begin = plan->wg_begin;
+    a.order = plan->order;
+    a.split_index = plan->split_index;
+    a.tiles_n = plan->host.tiles_n;
+  }
   a.M = M;
   a.N = N;
   a.K = K;
-  a.tiles_n = plan->host.tiles_n;
   a.win_m0 = m0;
   a.win_m1 = m1;
   a.win_n0 = n0;
@@ -408,6 +430,8 @@ const char* comet_status_str(comet_status_t s) {
 }
 
 const char* comet_last_error(void) { return g_last_error.c_str(); }
+
+const char* comet_build_stamp(void) { return kStamp + sizeof("COMET_SOURCE_STAMP=") - 1; }
 
 size_t comet_act_packed_bytes(const uint8_t* prec, int M, int K, int G) {
   if (!prec || M < 1 || G < 1 || K < G || K % G) return 0;
@@ -640,6 +664,15 @@ comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* p
   if (order)
     for (int i = 0; i < K / G; ++i) order[i] = plan.order[i];
   return ok();
+}
+
+int comet_gemm_kernel(int M, int N, int K, int G, int num_cus) {
+  if (M < 1 || N < 16 || N % 16 || num_cus < 1) {
+    fail(COMET_ERR_INVALID_ARG, "M=%d, N=%d, num_cus=%d: bad shape or CU count", M, N, num_cus);
+    return -1;
+  }
+  if (check_kg(K, G)) return -1;
+  return kernel_kind(M, N, K, num_cus);
 }
 
 void comet_release_caches(void) {

@@ -136,6 +136,17 @@ struct KBlock {
 
 __device__ __forceinline__ KBlock kblock(int e) { return KBlock{e & 1023, ((e >> 10) & 1) != 0, e >> 11}; }
 
+// End of the run of K-blocks of equal precision that starts at schedule
+// position pos (an LDS copy of the order; the run ends at `end` at the
+// latest).  The precision-batched order has two runs, 4-bit then 8-bit; the
+// natural order has as many as the map.
+__device__ __forceinline__ int run_end(const int* order, int pos, int end) {
+  const int b = __builtin_amdgcn_readfirstlane(order[pos]) & 1024;
+  int e = pos + 1;
+  while (e < end && (__builtin_amdgcn_readfirstlane(order[e]) & 1024) == b) ++e;
+  return e;
+}
+
 // The plan (schedule, work units, split table) is read-only while the kernel
 // runs.  Reading it through the constant address space keeps its loads on the
 // scalar unit: a vector load here would come with a wait on the vector-memory
@@ -699,13 +710,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
       }
     }
     barrier_lds();
-    const int split = min(max(p.n4, unit.g_begin), unit.g_end);
-    if (unit.g_begin < split)
-      kloop<TM, DIAG, false>(p, o, smem, lds, s_order, unit.g_begin, unit.g_begin, split,
-                             unit.g_end, NG, m0, n0, wp, wvoff, C);
-    if (split < unit.g_end)
-      kloop<TM, DIAG, true>(p, o, smem, lds, s_order, unit.g_begin, split, unit.g_end, unit.g_end,
-                            NG, m0, n0, wp, wvoff, C);
+    // one K-loop per run of equal precision; the loads run on across runs
+    for (int pos = unit.g_begin; pos < unit.g_end;) {
+      const int end = run_end(s_order, pos, unit.g_end);
+      if (s_order[pos] & 1024)
+        kloop<TM, DIAG, true>(p, o, smem, lds, s_order, unit.g_begin, pos, end, unit.g_end, NG,
+                              m0, n0, wp, wvoff, C);
+      else
+        kloop<TM, DIAG, false>(p, o, smem, lds, s_order, unit.g_begin, pos, end, unit.g_end, NG,
+                               m0, n0, wp, wvoff, C);
+      pos = end;
+    }
     if (DIAG) continue;
 
     store_tile<TM, SWIGLU>(p, unit, m0, n0, C, &s_last, smem);
@@ -892,9 +907,14 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
       mid_store(st, k0.b8, smem);
     }
     barrier_lds();
-    const int split = min(max(p.n4, gb), ge);
-    if (gb < split) mid_loop<DIAG, false>(p, o, smem, lds, s_order, gb, split, gb, ge, NG, m0, n0, st, C);
-    if (split < ge) mid_loop<DIAG, true>(p, o, smem, lds, s_order, split, ge, gb, ge, NG, m0, n0, st, C);
+    for (int pos = gb; pos < ge;) {
+      const int end = run_end(s_order, pos, ge);
+      if (s_order[pos] & 1024)
+        mid_loop<DIAG, true>(p, o, smem, lds, s_order, pos, end, gb, ge, NG, m0, n0, st, C);
+      else
+        mid_loop<DIAG, false>(p, o, smem, lds, s_order, pos, end, gb, ge, NG, m0, n0, st, C);
+      pos = end;
+    }
     if (DIAG) continue;
 
     store_tile<TM, SWIGLU>(p, unit, m0, n0, C, &s_last, smem);

@@ -539,7 +539,7 @@ hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream) 
   // is faster: it needs fewer registers (four waves per SIMD against three),
   // and with so few rows its activation reads cost little.
   const int R = (a.M + 15) / 16;
-  if (a.M > 8 && R <= 2 && a.splits <= 2) {
+  if (skinny_shared(a.M, a.splits)) {
     if (R == 1)
       return a.splits == 1 ? launch_shared<1, 1>(a, diag, stream) : launch_shared<1, 2>(a, diag, stream);
     return a.splits == 1 ? launch_shared<2, 1>(a, diag, stream) : launch_shared<2, 2>(a, diag, stream);

@@ -39,7 +39,6 @@ struct GemmArgs {
   const WorkUnit* units;
   const int* wg_begin;
   const int* order;   // K-block schedule, K/G (+ kOrderPad) entries: g | is8 << 10 | (g + 8-bit blocks before g) << 11
-  int n4;             // number of 4-bit blocks (they come first in `order`)
   const int* split_index;  // tile -> index into the partial/counter arrays (-1: not split)
   int M, N, K;
   int tiles_n;        // tiles along N
@@ -87,8 +86,11 @@ hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, i
 // and FMPQ quantization of h [M][I] with `map` into A / sa [I/G][M].
 hipError_t launch_swiglu_quantize(const uint16_t* GU, uint8_t* A, uint16_t* sa, int M, int I,
                                   const BlockMap& map, hipStream_t stream);
-// Few-token kernel (M <= kSkinnyMaxM): one wave per (16 columns, split-K slot).
+// Few-token kernels (M <= kSkinnyMaxM): one wave per (16 columns, split-K
+// slot), or, for 8 < M <= 32 with at most two slots, four column blocks per
+// workgroup sharing the activation operand through LDS.
 constexpr int kSkinnyMaxM = 48;
+inline bool skinny_shared(int M, int splits) { return M > 8 && M <= 32 && splits <= 2; }
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
 // Split-K slots (1, 2 or 4) for the few-token kernel: spread the (N/16 x
 // slots) waves evenly over the device's SIMDs, keeping at least 4 K-blocks per

@@ -57,17 +57,24 @@ bool build_plan(int M, int N, int K, int G, const uint8_t* prec, const PlanOptio
   const int P = opt.num_cus * opt.wgs_per_cu;
   const int xcds = opt.num_cus % 32 == 0 ? opt.num_cus / 32 : 1;
 
+  if (opt.mode != "dp" && opt.mode != "cost" && opt.mode != "natural") {
+    if (err) *err = "build_plan: unknown mode " + opt.mode;
+    return false;
+  }
   // K-block order: precision-batched (all 4-bit blocks, then all 8-bit ones),
-  // so a split unit switches precision at most once.
+  // so every tile's loop has at most two uniform phases and a split unit
+  // switches precision at most once.  "natural" keeps the map's own order
+  // (the baseline without tile remapping).
   for (int g = 0; g < NG; ++g) {
     if (prec[g] != 4 && prec[g] != 8) {
       if (err) *err = "build_plan: map entry not 4 or 8";
       return false;
     }
-    if (prec[g] == 4) p.order.push_back(g);
+    if (prec[g] == 4 || opt.mode == "natural") p.order.push_back(g);
   }
-  for (int g = 0; g < NG; ++g)
-    if (prec[g] == 8) p.order.push_back(g);
+  if (opt.mode != "natural")
+    for (int g = 0; g < NG; ++g)
+      if (prec[g] == 8) p.order.push_back(g);
   std::vector<double> prefix(NG + 1, 0.0);
   for (int i = 0; i < NG; ++i)
     prefix[i + 1] = prefix[i] + (prec[p.order[i]] == 8 ? opt.cost8 : opt.cost4);
@@ -89,9 +96,6 @@ bool build_plan(int M, int N, int K, int G, const uint8_t* prec, const PlanOptio
       const int full = T / P;
       dp_tiles = full >= 1 ? (full - 1) * P : 0;
     }
-  } else if (opt.mode != "dp" && opt.mode != "cost") {
-    if (err) *err = "build_plan: unknown mode " + opt.mode;
-    return false;
   }
   const int sk_tiles = T - dp_tiles;
   // Number of workgroups: enough for the data-parallel waves; the split part

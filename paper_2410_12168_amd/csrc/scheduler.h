@@ -31,7 +31,7 @@ struct Plan {
   int tile_m = 0, tile_n = 0;
   int tiles_m = 0, tiles_n = 0;
   int num_wgs = 0;             // persistent workgroups launched
-  std::vector<int> order;      // K-block processing order (all 4-bit, then all 8-bit)
+  std::vector<int> order;      // K-block processing order (all 4-bit, then all 8-bit; natural: 0..NG-1)
   std::vector<PlanUnit> units; // grouped by workgroup
   std::vector<int> wg_begin;   // num_wgs + 1 offsets into units
   std::vector<int> split_base; // per tile: first partial slot index, or -1 if unsplit
@@ -51,8 +51,12 @@ struct PlanOptions {
   // "cost" mode splits the last wave of tiles only if leaving it unsplit
   // would idle more than this share of the workgroups
   double split_min_idle = 0.3;
-  // "dp": one whole tile per unit, tiles dealt round-robin;
-  // "cost": data-parallel full waves + cost-balanced split of the remainder.
+  // "natural": the map's own K-block order, one whole tile per unit (no tile
+  //            remapping, no tile decomposition);
+  // "dp": precision-batched order, one whole tile per unit, tiles dealt
+  //       round-robin;
+  // "cost": precision-batched order, data-parallel full waves + cost-balanced
+  //         split of the remainder.
   std::string mode = "cost";
 };
 

@@ -1,0 +1,177 @@
+"""GPU parity where it was thin: every row tile of the full-size layers, the
+exact per-block sums of a split tile under the production schedule, the
+quantizer's edge rows fed through the GEMM, the wide-N rule for 33-48 rows,
+and the schedule modes (which must change nothing but the fp32 summation
+order).  Everything is compared with the CPU oracle: packed bytes and int32
+sums bit-exactly, fp16 outputs within the tolerance of tests/parity.py.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2410_12168_amd as comet
+import synth
+from parity import act_rows, assert_out_close
+from test_gpu_parity import DEV, dev_u16, host, host_u16, run_path
+
+pytestmark = pytest.mark.gpu
+
+
+def tile_rows(M, tile=256, seed=0):
+    """One token row inside every `tile`-row tile (at a seeded offset), plus
+    the first and last rows."""
+    rng = np.random.default_rng(seed)
+    rows = [t * tile + int(rng.integers(0, tile)) for t in range((M + tile - 1) // tile)]
+    return np.unique(np.clip(rows + [0, M - 1], 0, M - 1))
+
+
+@pytest.mark.parametrize("model,layer", [("70b", "qkv"), ("70b", "o"), ("70b", "gate_up"),
+                                         ("70b", "down"), ("8b", "gate_up"), ("8b", "down")])
+def test_one_row_per_row_tile_full_size(model, layer):
+    shapes, M = (synth.LLAMA3_70B, 4096) if model == "70b" else (synth.LLAMA3_8B, 2048)
+    K, N = shapes[layer]
+    NG = K // 128
+    print(f"row tiles {model} {layer} M={M} N={N} K={K}", flush=True)
+    prec = synth.prec_map(NG, NG // 16)
+    r = run_path(M, N, K, prec, seed=21)
+    rows = tile_rows(M, seed=NG)
+    qa, sa = oracle.quantize_act(r["X16"][rows], prec)
+    assert np.array_equal(act_rows(host(r["A"]), prec, M, rows), oracle.pack_act(qa, prec))
+    qw, sw = oracle.quantize_weight(r["W16"])
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16)[rows], ref, f"{model} {layer}")
+
+
+def test_split_tile_acc_window_production_plan():
+    """LLaMA-3-70B qkv at M = 4096: 640 tiles on 256 CUs, so the default
+    schedule splits the last wave.  The diagnostic entry point runs the same
+    schedule; a window inside a split tile must hold the exact block sums."""
+    K, N = synth.LLAMA3_70B["qkv"]
+    M, NG = 4096, K // 128
+    prec = synth.prec_map(NG, NG // 16)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    os.environ.pop("COMET_SCHED", None)
+    q = comet.comet_schedule_query(M, N, K, prec, num_cus=cus)
+    split = q["units"][q["units"][:, 4] > 1]
+    assert len(split) > 0, "expected a split last wave"
+    tile = int(split[len(split) // 2, 0])
+    tiles_n = (N + 255) // 256
+    m0, n0 = (tile // tiles_n) * 256, (tile % tiles_n) * 256
+    win = (m0 + 100, m0 + 132, n0 + 200, n0 + 256)  # crosses wave quadrants
+    print(f"split tile {tile} window {win}", flush=True)
+    r = run_path(M, N, K, prec, seed=31, diag_window=win)
+    rows = np.arange(win[0], win[1])
+    qa, sa = oracle.quantize_act(r["X16"][rows], prec)
+    qw, sw = oracle.quantize_weight(r["W16"][win[2]:win[3]])
+    assert np.array_equal(host(r["acc"]), oracle.group_acc(qa, qw))
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    out = host_u16(r["out"]).view(np.float16)[win[0]:win[1], win[2]:win[3]]
+    assert_out_close(out, ref, "split tile window")
+
+
+@pytest.mark.parametrize("M,N", [(6, 64), (6, 512), (70, 256), (300, 512)])
+def test_quantizer_edge_rows_through_gemm(M, N):
+    """Zero blocks, subnormal-scale blocks, exact ties and +-65504 in an 8-bit
+    block, quantized and contracted; every kernel regime (few-token, 128-row,
+    256-row tiles) sees them."""
+    K = 512
+    prec = np.array([4, 8, 4, 8], np.uint8)
+    rng = np.random.default_rng(M + N)
+    X = rng.standard_normal((M, K)).astype(np.float32)
+    X[0::6, :] = 0.0                           # all-zero rows
+    X[1::6, :] = 2.0 ** -24                    # smallest subnormal: subnormal scales
+    X[2::6, :128] = 0.0
+    X[2::6, :8] = [7.0, 2.5, -2.5, 3.5, 0.5, -0.5, 1.5, -1.5]  # ties (scale 1)
+    X[3::6, 128:256] *= 0.01
+    X[3::6, 128:130] = [65504.0, -65504.0]     # 8-bit block at the fp16 limit
+    X[4::6, 256:384] = 0.0                     # one zero block in a live row
+    X[5::6, 384:] = -(2.0 ** -20)
+    X16 = X.astype(np.float16).view(np.uint16)
+    W16 = synth.weights(M, N, K)
+    print(f"edge rows M={M} N={N}", flush=True)
+    A, sa = comet.quantize_act(dev_u16(X16), prec)
+    Wp, sw = comet.pack_w4(dev_u16(W16))
+    out = comet.w4ax_gemm(A, prec, sa, Wp, sw, M, N, K)
+    acc = comet.w4ax_gemm_acc(A, prec, sa, Wp, sw, M, N, K, 0, M, 0, N)
+    qa, osa = oracle.quantize_act(X16, prec)
+    qw, osw = oracle.quantize_weight(W16)
+    assert np.array_equal(host_u16(sa), osa)
+    assert np.array_equal(host(A), oracle.pack_act(qa, prec))
+    assert np.array_equal(host(acc), oracle.group_acc(qa, qw))
+    ref = oracle.dequant_gemm(qa, osa, qw, osw)
+    assert np.abs(ref).max() < 60000.0  # the reference itself fits fp16
+    assert_out_close(host_u16(out).view(np.float16), ref, f"edge rows {M}x{N}")
+
+
+@pytest.mark.parametrize("M", [33, 48])
+def test_wide_n_mid_rows_acc_window(M):
+    """LLaMA-3-70B gate_up at 33 and 48 rows runs on the 128-row tile kernel
+    (its 224 column tiles are wide): exact block sums over every row and a
+    column window across a tile boundary, and sampled fp16 rows."""
+    K, N = synth.LLAMA3_70B["gate_up"]
+    NG = K // 128
+    assert comet.comet_gemm_kernel(M, N, K, 256) == 2
+    prec = synth.prec_map(NG, NG // 16)
+    win = (0, M, 256 * 100 - 24, 256 * 100 + 40)
+    print(f"wide-N M={M} window {win}", flush=True)
+    r = run_path(M, N, K, prec, seed=M, diag_window=win)
+    qa, sa = oracle.quantize_act(r["X16"], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    assert np.array_equal(host(r["acc"]), oracle.group_acc(qa, qw[win[2]:win[3]]))
+    rows = np.array([0, M // 2, M - 1])
+    ref = oracle.dequant_gemm(qa[rows], sa[:, rows], qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16)[rows], ref, f"wide-N M={M}")
+
+
+def test_fused_swiglu_wide_n_mid_rows():
+    """The fused SwiGLU entry point at M = 40 on the 70B gate_up shape (the
+    128-row kernel's fused epilogue) against the oracle's SwiGLU quantization
+    of the same GEMM's fp16 output."""
+    M, (K, N) = 40, synth.LLAMA3_70B["gate_up"]
+    I = N // 2
+    NG = K // 128
+    print(f"fused swiglu wide-N M={M}", flush=True)
+    prec = synth.prec_map(NG, NG // 16)
+    A, sa = comet.quantize_act(dev_u16(synth.activations(40, M, K, prec)), prec)
+    Wp, sw = comet.pack_w4(dev_u16(synth.weights(40, N, K)))
+    out_map = synth.prec_map(I // 128, I // 128 // 16, "random", seed=3)
+    A2, sa2 = comet.w4ax_gemm_swiglu_quant(A, prec, sa, Wp, sw, M, N, K, out_map)
+    out = comet.w4ax_gemm(A, prec, sa, Wp, sw, M, N, K)
+    A_ref, sa_ref = oracle.swiglu_quantize(host_u16(out), out_map)
+    assert np.array_equal(host_u16(sa2), sa_ref)
+    assert np.array_equal(host(A2), A_ref)
+
+
+@pytest.mark.parametrize("M,N,K,placement", [(4096, 10240, 8192, "random"),
+                                             (300, 1024, 4096, "contiguous"),
+                                             (100, 2048, 2048, "random")])
+def test_schedule_modes_agree(M, N, K, placement):
+    """natural (map order, whole tiles), dp (precision-batched, whole tiles)
+    and cost (precision-batched, split last wave) give bit-identical block
+    sums and outputs within the oracle tolerance."""
+    NG = K // 128
+    prec = synth.prec_map(NG, NG // 4, placement, seed=K)
+    X16 = synth.activations(7, M, K, prec)
+    W16 = synth.weights(7, N, K)
+    A, sa = comet.quantize_act(dev_u16(X16), prec)
+    Wp, sw = comet.pack_w4(dev_u16(W16))
+    win = (M - 20, M, N - 24, N)
+    rows = np.array([0, M // 3, M - 1])
+    qa, osa = oracle.quantize_act(X16[rows], prec)
+    qw, osw = oracle.quantize_weight(W16)
+    ref = oracle.dequant_gemm(qa, osa, qw, osw)
+    qa_w, _ = oracle.quantize_act(X16[win[0]:win[1]], prec)
+    acc_ref = oracle.group_acc(qa_w, qw[win[2]:win[3]])
+    try:
+        for mode in ("natural", "dp", "cost"):
+            print(f"schedule mode {mode} M={M} N={N} K={K}", flush=True)
+            os.environ["COMET_SCHED"] = mode
+            out = comet.w4ax_gemm(A, prec, sa, Wp, sw, M, N, K)
+            acc = comet.w4ax_gemm_acc(A, prec, sa, Wp, sw, M, N, K, *win)
+            assert np.array_equal(host(acc), acc_ref), mode
+            assert_out_close(host_u16(out).view(np.float16)[rows], ref, f"mode {mode}")
+    finally:
+        os.environ.pop("COMET_SCHED", None)
