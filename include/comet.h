@@ -66,8 +66,8 @@
  *     data-parallel full waves of tiles, the last wave split by cost),
  *     "dp" (precision-batched order, whole tiles only) or "natural" (the
  *     map's own K order, whole tiles only: no tile remapping and no tile
- *     decomposition).  Results do not depend on the mode beyond the fp32
- *     summation order.
+ *     decomposition; the fused SwiGLU entry point takes "dp" instead).
+ *     Results do not depend on the mode beyond the fp32 summation order.
  */
 #ifndef COMET_H
 #define COMET_H

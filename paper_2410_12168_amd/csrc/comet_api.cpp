@@ -358,8 +358,10 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   const bool skinny = kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED;
   // the few-token kernels walk the K-blocks in natural order and need no plan
   const DevicePlan* plan = nullptr;
-  if (!skinny &&
-      (st = get_plan(dev, info.cus, M, N, K, prec, map, sched_mode(), stream, &plan)))
+  // the fused SwiGLU epilogue has no natural-order form: it takes "dp" instead
+  std::string mode = sched_mode();
+  if (swiglu && mode == "natural") mode = "dp";
+  if (!skinny && (st = get_plan(dev, info.cus, M, N, K, prec, map, mode, stream, &plan)))
     return st;
   comet::GemmArgs a{};
   a.splits = skinny ? comet::skinny_splits(N, K, info.cus) : 1;
@@ -386,6 +388,8 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
     a.split_index = plan->split_index;
     a.tiles_n = plan->host.tiles_n;
   }
+  a.n4 = 0;
+  for (int g = 0; g < K / comet::kG; ++g) a.n4 += prec[g] == 4;
   a.M = M;
   a.N = N;
   a.K = K;
@@ -410,7 +414,7 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   }
   if (skinny) return launched(comet::launch_gemm_skinny(a, diag, stream), "gemm launch");
   return launched(comet::launch_gemm(a, plan->host.num_wgs, diag, swiglu != nullptr,
-                                     plan->host.tile_m, stream),
+                                     mode == "natural", plan->host.tile_m, stream),
                   "gemm launch");
 }
 

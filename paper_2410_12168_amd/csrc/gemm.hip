@@ -663,7 +663,9 @@ __device__ __forceinline__ void store_tile(const GemmArgs& p, const WorkUnit& un
     }
 }
 
-template <int TM, bool DIAG, bool SWIGLU>
+// NAT: the schedule lists the K-blocks in the map's own order (the ablation
+// baseline without tile remapping); otherwise all 4-bit blocks come first.
+template <int TM, bool DIAG, bool SWIGLU, bool NAT>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
   constexpr int kRB = Geo<TM>::RB, kBuf = Geo<TM>::Buf;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -710,16 +712,30 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
       }
     }
     barrier_lds();
-    // one K-loop per run of equal precision; the loads run on across runs
-    for (int pos = unit.g_begin; pos < unit.g_end;) {
-      const int end = run_end(s_order, pos, unit.g_end);
-      if (s_order[pos] & 1024)
-        kloop<TM, DIAG, true>(p, o, smem, lds, s_order, unit.g_begin, pos, end, unit.g_end, NG,
-                              m0, n0, wp, wvoff, C);
-      else
-        kloop<TM, DIAG, false>(p, o, smem, lds, s_order, unit.g_begin, pos, end, unit.g_end, NG,
-                               m0, n0, wp, wvoff, C);
-      pos = end;
+    if constexpr (NAT) {
+      // natural order: one K-loop per run of equal precision, the loads
+      // running on across runs
+      for (int pos = unit.g_begin; pos < unit.g_end;) {
+        const int end = run_end(s_order, pos, unit.g_end);
+        if (s_order[pos] & 1024)
+          kloop<TM, DIAG, true>(p, o, smem, lds, s_order, unit.g_begin, pos, end, unit.g_end, NG,
+                                m0, n0, wp, wvoff, C);
+        else
+          kloop<TM, DIAG, false>(p, o, smem, lds, s_order, unit.g_begin, pos, end, unit.g_end,
+                                 NG, m0, n0, wp, wvoff, C);
+        pos = end;
+      }
+    } else {
+      // precision-batched order: the 4-bit run, then the 8-bit run, as two
+      // straight-line loops (a loop over runs holding both bodies makes the
+      // register allocator spill)
+      const int split = min(max(p.n4, unit.g_begin), unit.g_end);
+      if (unit.g_begin < split)
+        kloop<TM, DIAG, false>(p, o, smem, lds, s_order, unit.g_begin, unit.g_begin, split,
+                               unit.g_end, NG, m0, n0, wp, wvoff, C);
+      if (split < unit.g_end)
+        kloop<TM, DIAG, true>(p, o, smem, lds, s_order, unit.g_begin, split, unit.g_end,
+                              unit.g_end, NG, m0, n0, wp, wvoff, C);
     }
     if (DIAG) continue;
 
@@ -866,7 +882,7 @@ __device__ __forceinline__ void mid_loop(const GemmArgs& p, const LaneOffsets& o
   }
 }
 
-template <bool DIAG, bool SWIGLU>
+template <bool DIAG, bool SWIGLU, bool NAT>
 __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
   constexpr int TM = kMidTM, kRB = Geo<TM>::RB;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -907,13 +923,21 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
       mid_store(st, k0.b8, smem);
     }
     barrier_lds();
-    for (int pos = gb; pos < ge;) {
-      const int end = run_end(s_order, pos, ge);
-      if (s_order[pos] & 1024)
-        mid_loop<DIAG, true>(p, o, smem, lds, s_order, pos, end, gb, ge, NG, m0, n0, st, C);
-      else
-        mid_loop<DIAG, false>(p, o, smem, lds, s_order, pos, end, gb, ge, NG, m0, n0, st, C);
-      pos = end;
+    if constexpr (NAT) {
+      for (int pos = gb; pos < ge;) {
+        const int end = run_end(s_order, pos, ge);
+        if (s_order[pos] & 1024)
+          mid_loop<DIAG, true>(p, o, smem, lds, s_order, pos, end, gb, ge, NG, m0, n0, st, C);
+        else
+          mid_loop<DIAG, false>(p, o, smem, lds, s_order, pos, end, gb, ge, NG, m0, n0, st, C);
+        pos = end;
+      }
+    } else {
+      const int split = min(max(p.n4, gb), ge);
+      if (gb < split)
+        mid_loop<DIAG, false>(p, o, smem, lds, s_order, gb, split, gb, ge, NG, m0, n0, st, C);
+      if (split < ge)
+        mid_loop<DIAG, true>(p, o, smem, lds, s_order, split, ge, gb, ge, NG, m0, n0, st, C);
     }
     if (DIAG) continue;
 
@@ -921,43 +945,43 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
   }
 }
 
+typedef void (*GemmKernelFn)(GemmArgs);
+
+// The instantiations: production (plain, diagnostic, SwiGLU epilogue) and the
+// natural-order ablation (plain, diagnostic), for both tile heights.
+GemmKernelFn gemm_kernel_fn(int tile_m, bool diag, bool swiglu, bool natural) {
+  if (tile_m == kMidTM) {
+    if (natural) return diag ? gemm_mid_kernel<true, false, true> : gemm_mid_kernel<false, false, true>;
+    if (diag) return gemm_mid_kernel<true, false, false>;
+    return swiglu ? gemm_mid_kernel<false, true, false> : gemm_mid_kernel<false, false, false>;
+  }
+  if (natural) return diag ? gemm_kernel<256, true, false, true> : gemm_kernel<256, false, false, true>;
+  if (diag) return gemm_kernel<256, true, false, false>;
+  return swiglu ? gemm_kernel<256, false, true, false> : gemm_kernel<256, false, false, false>;
+}
+
 }  // namespace
 
 int gemm_lds_bytes(int tile_m) { return tile_m == kMidTM ? kMidLds : Geo<256>::Lds; }
 
-hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, int tile_m,
-                       hipStream_t stream) {
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, bool natural,
+                       int tile_m, hipStream_t stream) {
   const dim3 grid(num_wgs), block(kThreads);
-  if (tile_m == kMidTM) {
-    if (diag)
-      hipLaunchKernelGGL((gemm_mid_kernel<true, false>), grid, block, kMidLds, stream, a);
-    else if (swiglu)
-      hipLaunchKernelGGL((gemm_mid_kernel<false, true>), grid, block, kMidLds, stream, a);
-    else
-      hipLaunchKernelGGL((gemm_mid_kernel<false, false>), grid, block, kMidLds, stream, a);
-  } else {
-    if (diag)
-      hipLaunchKernelGGL((gemm_kernel<256, true, false>), grid, block, Geo<256>::Lds, stream, a);
-    else if (swiglu)
-      hipLaunchKernelGGL((gemm_kernel<256, false, true>), grid, block, Geo<256>::Lds, stream, a);
-    else
-      hipLaunchKernelGGL((gemm_kernel<256, false, false>), grid, block, Geo<256>::Lds, stream, a);
-  }
+  if (swiglu && natural) return hipErrorInvalidValue;  // not instantiated
+  const int lds = tile_m == kMidTM ? kMidLds : Geo<256>::Lds;
+  hipLaunchKernelGGL(gemm_kernel_fn(tile_m, diag, swiglu, natural), grid, block, lds, stream, a);
   return hipGetLastError();
 }
 
 hipError_t set_gemm_attributes() {
-  const void* fns[6] = {reinterpret_cast<const void*>(&gemm_kernel<256, false, false>),
-                        reinterpret_cast<const void*>(&gemm_kernel<256, true, false>),
-                        reinterpret_cast<const void*>(&gemm_kernel<256, false, true>),
-                        reinterpret_cast<const void*>(&gemm_mid_kernel<false, false>),
-                        reinterpret_cast<const void*>(&gemm_mid_kernel<true, false>),
-                        reinterpret_cast<const void*>(&gemm_mid_kernel<false, true>)};
-  const int lds[6] = {Geo<256>::Lds, Geo<256>::Lds, Geo<256>::Lds, kMidLds, kMidLds, kMidLds};
-  for (int i = 0; i < 6; ++i) {
-    hipError_t e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, lds[i]);
-    if (e != hipSuccess) return e;
-  }
+  for (int tm : {256, kMidTM})
+    for (int v = 0; v < 5; ++v) {
+      const bool diag = v == 1 || v == 4, swiglu = v == 2, natural = v >= 3;
+      hipError_t e = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(gemm_kernel_fn(tm, diag, swiglu, natural)),
+          hipFuncAttributeMaxDynamicSharedMemorySize, tm == kMidTM ? kMidLds : Geo<256>::Lds);
+      if (e != hipSuccess) return e;
+    }
   return hipSuccess;
 }
 

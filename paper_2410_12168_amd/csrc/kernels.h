@@ -39,6 +39,7 @@ struct GemmArgs {
   const WorkUnit* units;
   const int* wg_begin;
   const int* order;   // K-block schedule, K/G (+ kOrderPad) entries: g | is8 << 10 | (g + 8-bit blocks before g) << 11
+  int n4;             // number of 4-bit blocks (they come first in `order`, except in natural order)
   const int* split_index;  // tile -> index into the partial/counter arrays (-1: not split)
   int M, N, K;
   int tiles_n;        // tiles along N
@@ -79,9 +80,11 @@ constexpr int kTileN = 256;
 inline int gemm_tile_m(int M) { return M <= kTileMSmall ? kTileMSmall : kTileM; }
 
 // Persistent GEMM: `num_wgs` workgroups walk a.units (a.wg_begin per group);
-// tile_m is gemm_tile_m(a.M); swiglu selects the SwiGLU + quantize epilogue.
-hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, int tile_m,
-                       hipStream_t stream);
+// tile_m is gemm_tile_m(a.M); swiglu selects the SwiGLU + quantize epilogue;
+// natural: the plan's K order is the map's own (not precision-batched), which
+// the SwiGLU epilogue does not support.
+hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, bool natural,
+                       int tile_m, hipStream_t stream);
 // SwiGLU of an fp16 gate/up output GU [M][2I] (2G-wide gate/up column groups)
 // and FMPQ quantization of h [M][I] with `map` into A / sa [I/G][M].
 hipError_t launch_swiglu_quantize(const uint16_t* GU, uint8_t* A, uint16_t* sa, int M, int I,
