@@ -210,6 +210,29 @@ COMET_API comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t*
                                const uint16_t* w_scales, uint16_t* out, int M, int N, int K,
                                int G, hipStream_t stream);
 
+/* comet_w4ax_gemm for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, results and errors; in addition:
+ *   - the library's device memory for this call (the tile kernels' schedule,
+ *     split-tile fp32 partials and arrival counters) is one static array per
+ *     device of 66 MiB + 64 KiB, held until the process ends; the call makes
+ *     no hipMalloc, hipFree or other allocating call;
+ *   - every call on a device shares that array: calls that overlap on one
+ *     device (e.g. on two streams) race and must not be issued;
+ *   - a schedule that would split tiles into more partials than the array
+ *     holds (64 MiB) runs with whole tiles instead (same results within the
+ *     fp32 summation order); a schedule larger than 2 MiB (about 87,000
+ *     output tiles) is refused with COMET_ERR_UNSUPPORTED;
+ *   - the first call after the schedule changes (a new shape, map or mode)
+ *     copies the schedule from host memory and waits for the copy; calls that
+ *     repeat the previous shape only enqueue kernels. */
+COMET_API comet_status_t comet_w4ax_gemm_noalloc(const uint8_t* A_packed,
+                                                 const uint8_t* group_prec_map,
+                                                 const uint16_t* a_scales,
+                                                 const uint8_t* W_packed,
+                                                 const uint16_t* w_scales, uint16_t* out, int M,
+                                                 int N, int K, int G, hipStream_t stream);
+
 /* SwiGLU and the next layer's quantization, fused into the W4Ax GEMM (the step
  * after the path: in a LLaMA MLP the gate/up GEMM's output feeds the down
  * projection through h = SiLU(gate) * up, whose activations FMPQ quantizes in

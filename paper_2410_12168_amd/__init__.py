@@ -74,6 +74,7 @@ def lib():
         "comet_w4ax_gemm_swiglu_quant": (I, [P, P, P, P, P, I, I, I, I, P, P, P, P]),
         "comet_swiglu_quantize": (I, [P, P, P, P, I, I, I, P]),
         "comet_gemm_kernel": (I, [I, I, I, I, I]),
+        "comet_w4ax_gemm_noalloc": (I, [P, P, P, P, P, P, I, I, I, I, P]),
         "comet_build_stamp": (ctypes.c_char_p, []),
         "comet_status_str": (ctypes.c_char_p, [I]),
         "comet_last_error": (ctypes.c_char_p, []),
@@ -288,6 +289,15 @@ def comet_w4ax_gemm(A_packed, group_prec_map, a_scales, W_packed, w_scales, out,
     _room(out, 2 * M * N, "out")
     _check(lib().comet_w4ax_gemm(_ptr(A_packed), _ptr(m), _ptr(a_scales), _ptr(W_packed),
                                  _ptr(w_scales), _ptr(out), M, N, K, G, _stream(stream)))
+
+
+def comet_w4ax_gemm_noalloc(A_packed, group_prec_map, a_scales, W_packed, w_scales, out, M: int,
+                            N: int, K: int, G: int = G, stream=None) -> None:
+    m = _map(group_prec_map, K, G)
+    _gemm_room(A_packed, m, a_scales, W_packed, w_scales, M, N, K, G)
+    _room(out, 2 * M * N, "out")
+    _check(lib().comet_w4ax_gemm_noalloc(_ptr(A_packed), _ptr(m), _ptr(a_scales), _ptr(W_packed),
+                                         _ptr(w_scales), _ptr(out), M, N, K, G, _stream(stream)))
 
 
 def comet_w4ax_gemm_acc(A_packed, group_prec_map, a_scales, W_packed, w_scales, acc, M: int,

@@ -23,8 +23,8 @@ OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcomet.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["quantize.hip", "gemm.hip", "gemm_skinny.hip", "kv4.hip", "scheduler.cpp", "calib.cpp",
-           "comet_api.cpp"]
+SOURCES = ["quantize.hip", "gemm.hip", "gemm_skinny.hip", "kv4.hip", "noalloc.hip", "scheduler.cpp",
+           "calib.cpp", "comet_api.cpp"]
 
 # The GEMM's inner loop interleaves MFMAs with the dequantization FMAs: keep
 # MFMA results in VGPRs (no accumulator-register copies).

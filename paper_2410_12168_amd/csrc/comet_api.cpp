@@ -194,6 +194,38 @@ comet::PlanOptions plan_options(int M, int cus, const std::string& mode) {
   return opt;
 }
 
+// A plan as the kernels read it, one int array: work units (5 ints each) |
+// wg_begin | K-block schedule (block index, precision bit and the block's
+// offset in A_packed in units of M*64 bytes, then kOrderPad repeats of the
+// last entry, since kernels prefetch fixed-size batches past the end of a
+// range) | split table.
+struct PlanBlob {
+  std::vector<int> v;
+  size_t o_wgb = 0, o_order = 0, o_split = 0;
+};
+
+PlanBlob plan_blob(const comet::Plan& h, const uint8_t* prec) {
+  PlanBlob b;
+  for (const comet::PlanUnit& u : h.units) {
+    b.v.push_back(u.tile);
+    b.v.push_back(u.g_begin);
+    b.v.push_back(u.g_end);
+    b.v.push_back(u.slot);
+    b.v.push_back(u.nslots);
+  }
+  b.o_wgb = b.v.size();
+  b.v.insert(b.v.end(), h.wg_begin.begin(), h.wg_begin.end());
+  b.o_order = b.v.size();
+  std::vector<int> n8_before(h.order.size() + 1, 0);
+  for (size_t g = 0; g < h.order.size(); ++g) n8_before[g + 1] = n8_before[g] + (prec[g] == 8);
+  for (int g : h.order) b.v.push_back(g | (prec[g] == 8) << 10 | (g + n8_before[g]) << 11);
+  const int last = b.v.back();
+  b.v.insert(b.v.end(), comet::kOrderPad, last);
+  b.o_split = b.v.size();
+  b.v.insert(b.v.end(), h.split_base.begin(), h.split_base.end());
+  return b;
+}
+
 // Plan for (device, shape, map, mode), built and uploaded on first use.
 // Caller holds g_mu.
 comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* prec,
@@ -209,31 +241,8 @@ comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* pr
   std::string err;
   if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, cus, mode), &dp.host, &err))
     return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
-  const comet::Plan& h = dp.host;
-  std::vector<int> blob;
-  for (const comet::PlanUnit& u : h.units) {
-    blob.push_back(u.tile);
-    blob.push_back(u.g_begin);
-    blob.push_back(u.g_end);
-    blob.push_back(u.slot);
-    blob.push_back(u.nslots);
-  }
-  const size_t o_wgb = blob.size();
-  blob.insert(blob.end(), h.wg_begin.begin(), h.wg_begin.end());
-  // K-block schedule as the kernel reads it: block index, precision bit and
-  // the block's offset in A_packed (in units of M*64 bytes)
-  const size_t o_order = blob.size();
-  {
-    std::vector<int> n8_before(h.order.size() + 1, 0);
-    for (size_t g = 0; g < h.order.size(); ++g) n8_before[g + 1] = n8_before[g] + (prec[g] == 8);
-    for (int g : h.order) blob.push_back(g | (prec[g] == 8) << 10 | (g + n8_before[g]) << 11);
-    // kernels prefetch fixed-size batches past the end of a range; the padding
-    // repeats the last entry so that such reads stay valid block addresses
-    const int last = blob.back();
-    blob.insert(blob.end(), comet::kOrderPad, last);
-  }
-  const size_t o_split = blob.size();
-  blob.insert(blob.end(), h.split_base.begin(), h.split_base.end());
+  const PlanBlob b = plan_blob(dp.host, prec);
+  const std::vector<int>& blob = b.v;
   if (std::getenv("COMET_TEST_FAIL_ALLOC")) return fail(COMET_ERR_OOM, "plan allocation failed (forced)");
   hipError_t e = hipMalloc(&dp.dmem, blob.size() * sizeof(int));
   if (e != hipSuccess) return fail(COMET_ERR_OOM, "plan allocation: %s", hipGetErrorString(e));
@@ -246,9 +255,10 @@ comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* pr
   }
   int* d = static_cast<int*>(dp.dmem);
   dp.units = reinterpret_cast<const comet::WorkUnit*>(d);
-  dp.wg_begin = d + o_wgb;
-  dp.order = d + o_order;
-  dp.split_index = d + o_split;
+  dp.wg_begin = d + b.o_wgb;
+  dp.order = d + b.o_order;
+  dp.split_index = d + b.o_split;
+  const comet::Plan& h = dp.host;
   if (std::getenv("COMET_LOG"))
     std::fprintf(stderr,
                  "[comet] plan M=%d N=%d K=%d mode=%s tiles=%dx%d wgs=%d units=%zu split_tiles=%d "
@@ -418,6 +428,99 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
                   "gemm launch");
 }
 
+// Per device: the plan last uploaded into the no-allocation workspace.
+std::map<int, std::vector<int>> g_noalloc_plan;
+
+// comet_w4ax_gemm over the fixed per-device workspace: no device allocation.
+// The few-token kernels need no workspace.  The tile kernels' plan goes into
+// the workspace's plan region (uploaded, with a wait, only when it differs
+// from the plan already there); split partials and counters use the other
+// regions, and a plan whose splits need more partials than fit is replaced
+// by the same mode's whole-tile plan.
+comet_status_t run_gemm_noalloc(const uint8_t* A, const uint8_t* prec, const uint16_t* sa,
+                                const uint8_t* W, const uint16_t* sw, uint16_t* out, int M, int N,
+                                int K, const comet::BlockMap& map, hipStream_t stream) {
+  int dev;
+  DeviceInfo info;
+  comet_status_t st = current_device(&dev, &info);
+  if (st) return st;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_attr_set[dev]) {
+    hipError_t e = comet::set_gemm_attributes();
+    if (e != hipSuccess) return fail(COMET_ERR_HIP, "kernel attributes: %s", hipGetErrorString(e));
+    g_attr_set[dev] = true;
+  }
+  const int kind = kernel_kind(M, N, K, info.cus);
+  comet::GemmArgs a{};
+  a.A = A;
+  a.sa = sa;
+  a.W = W;
+  a.sw = sw;
+  a.out = out;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.map = map;
+  for (int g = 0; g < K / comet::kG; ++g) a.n4 += prec[g] == 4;
+  if (kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED) {
+    a.splits = comet::skinny_splits(N, K, info.cus);
+    return launched(comet::launch_gemm_skinny(a, false, stream), "gemm launch");
+  }
+  uint8_t* ws = nullptr;
+  hipError_t e = comet::noalloc_scratch(dev, &ws);
+  if (e != hipSuccess)
+    return fail(COMET_ERR_HIP, "workspace address (hipGetSymbolAddress): %s", hipGetErrorString(e));
+  std::string mode = sched_mode();
+  comet::Plan h;
+  std::string err;
+  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, info.cus, mode), &h, &err))
+    return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
+  const size_t tile_bytes = (size_t)h.tile_m * h.tile_n * sizeof(float);
+  if ((size_t)h.partial_slots * tile_bytes > comet::kNoallocPartialBytes ||
+      (size_t)h.partial_slots * sizeof(int) > comet::kNoallocCounterBytes) {
+    mode = "dp";
+    if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, info.cus, mode), &h, &err))
+      return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
+  }
+  const PlanBlob b = plan_blob(h, prec);
+  const size_t plan_bytes = b.v.size() * sizeof(int);
+  if (plan_bytes > comet::kNoallocPlanBytes)
+    return fail(COMET_ERR_UNSUPPORTED,
+                "M=%d, N=%d, K=%d: the schedule takes %zu bytes, more than the %zu of the "
+                "no-allocation workspace (use comet_w4ax_gemm)",
+                M, N, K, plan_bytes, comet::kNoallocPlanBytes);
+  float* partials = reinterpret_cast<float*>(ws);
+  int* counters = reinterpret_cast<int*>(ws + comet::kNoallocPartialBytes);
+  int* plan = reinterpret_cast<int*>(ws + comet::kNoallocPartialBytes + comet::kNoallocCounterBytes);
+  std::vector<int>& cur = g_noalloc_plan[dev];
+  if (cur != b.v) {
+    // the copy reads pageable host memory: wait for it before the vector can change
+    e = hipMemcpyAsync(plan, b.v.data(), plan_bytes, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) {
+      cur.clear();
+      return fail(COMET_ERR_HIP, "plan upload: %s", hipGetErrorString(e));
+    }
+    cur = b.v;
+  }
+  // split tiles count arrivals from zero (a fill kernel, not a memset, so the
+  // call can be captured in a graph)
+  if (h.partial_slots > 0 &&
+      (st = launched(comet::launch_zero_ints(counters, h.partial_slots, stream), "counter reset")))
+    return st;
+  a.partials = partials;
+  a.counters = counters;
+  a.units = reinterpret_cast<const comet::WorkUnit*>(plan);
+  a.wg_begin = plan + b.o_wgb;
+  a.order = plan + b.o_order;
+  a.split_index = plan + b.o_split;
+  a.tiles_n = h.tiles_n;
+  a.splits = 1;
+  return launched(comet::launch_gemm(a, h.num_wgs, false, false, mode == "natural", h.tile_m,
+                                     stream),
+                  "gemm launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -568,6 +671,17 @@ comet_status_t comet_w4ax_gemm(const uint8_t* A_packed, const uint8_t* prec,
   if (st) return st;
   return run_gemm(A_packed, prec, a_scales, W_packed, w_scales, out, nullptr, M, N, K, map, 0, 0,
                   0, 0, stream);
+}
+
+comet_status_t comet_w4ax_gemm_noalloc(const uint8_t* A_packed, const uint8_t* prec,
+                                       const uint16_t* a_scales, const uint8_t* W_packed,
+                                       const uint16_t* w_scales, uint16_t* out, int M, int N,
+                                       int K, int G, hipStream_t stream) {
+  comet::BlockMap map;
+  comet_status_t st =
+      gemm_common(A_packed, prec, a_scales, W_packed, w_scales, out, M, N, K, G, &map);
+  if (st) return st;
+  return run_gemm_noalloc(A_packed, prec, a_scales, W_packed, w_scales, out, M, N, K, map, stream);
 }
 
 comet_status_t comet_w4ax_gemm_swiglu_quant(const uint8_t* A_packed, const uint8_t* prec,

@@ -100,6 +100,20 @@ hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
 // slot.
 int skinny_splits(int N, int K, int cus);
 
+// Fixed per-device workspace of the no-allocation GEMM entry point:
+// [fp32 split partials][split arrival counters][plan], in one static device
+// array (noalloc.hip).  64 MiB of partials holds the split plans of the
+// LLaMA-3 shapes (256 slots of a 256 x 256 tile); 2 MiB of plan holds about
+// 87,000 tiles (six ints per tile).
+constexpr size_t kNoallocPartialBytes = size_t(64) << 20;
+constexpr size_t kNoallocCounterBytes = size_t(64) << 10;
+constexpr size_t kNoallocPlanBytes = size_t(2) << 20;
+constexpr size_t kNoallocBytes = kNoallocPartialBytes + kNoallocCounterBytes + kNoallocPlanBytes;
+// Device address of the current device `dev`'s workspace (looked up once per
+// device, with that device current).
+hipError_t noalloc_scratch(int dev, uint8_t** ptr);
+hipError_t launch_zero_ints(int* p, int n, hipStream_t stream);
+
 // Allows the GEMM's dynamic LDS size; once per process and device.
 hipError_t set_gemm_attributes();
 int gemm_lds_bytes(int tile_m);
