@@ -293,12 +293,16 @@ __device__ __forceinline__ void act_dma(const GemmArgs& p, const KBlock& kb, int
 // into activation stage `buf` (FP8 bytes, swizzled rows).
 __device__ __forceinline__ void act_unpack(const uint8_t* raw, uint8_t* buf) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // all four reads first: one LDS round trip instead of four
+  u32x4 v[4];
+  #pragma unroll
+  for (int i = 0; i < 4; ++i)
+    v[i] = *reinterpret_cast<const u32x4*>(raw + (4 * wave + i) * 1024 + lane * 16);
   #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = 64 * wave + 16 * i + (lane >> 2), c = lane & 3;
-    const u32x4 v = *reinterpret_cast<const u32x4*>(raw + (4 * wave + i) * 1024 + lane * 16);
     u32x4 lo, hi;
-    unpack4(v, lo, hi);
+    unpack4(v[i], lo, hi);
     *reinterpret_cast<u32x4*>(buf + swz(r, 2 * c)) = lo;
     *reinterpret_cast<u32x4*>(buf + swz(r, 2 * c + 1)) = hi;
   }
