@@ -360,6 +360,7 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_attr_set[dev]) {
     hipError_t e = comet::set_gemm_attributes();
+    if (e == hipSuccess) e = comet::set_skinny_attributes();
     if (e != hipSuccess) return fail(COMET_ERR_HIP, "kernel attributes: %s", hipGetErrorString(e));
     g_attr_set[dev] = true;
   }
@@ -403,6 +404,7 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   a.M = M;
   a.N = N;
   a.K = K;
+  a.cus = info.cus;
   a.win_m0 = m0;
   a.win_m1 = m1;
   a.win_n0 = n0;
@@ -447,6 +449,7 @@ comet_status_t run_gemm_noalloc(const uint8_t* A, const uint8_t* prec, const uin
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_attr_set[dev]) {
     hipError_t e = comet::set_gemm_attributes();
+    if (e == hipSuccess) e = comet::set_skinny_attributes();
     if (e != hipSuccess) return fail(COMET_ERR_HIP, "kernel attributes: %s", hipGetErrorString(e));
     g_attr_set[dev] = true;
   }
@@ -460,6 +463,7 @@ comet_status_t run_gemm_noalloc(const uint8_t* A, const uint8_t* prec, const uin
   a.M = M;
   a.N = N;
   a.K = K;
+  a.cus = info.cus;
   a.map = map;
   for (int g = 0; g < K / comet::kG; ++g) a.n4 += prec[g] == 4;
   if (kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED) {

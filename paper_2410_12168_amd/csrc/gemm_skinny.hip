@@ -531,9 +531,378 @@ hipError_t launch_shared(const GemmArgs& a, bool diag, hipStream_t stream) {
   return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------
+// Few-token stream kernel (M <= 8).  W_packed's 16-row panels make the whole
+// weight matrix one contiguous run of 1 KB items, item p * NG + g being panel
+// p's K-block g.  Each workgroup owns kp whole panels and its 16 waves split
+// the workgroup's kp * NG items into contiguous ranges, so every wave streams
+// one long run of W_packed (56 KB for the LLaMA-3-70B gate_up), four items
+// per batch with the next batch in flight, and the grid is exactly one wave
+// of workgroups (no tail round).  A wave accumulates one panel at a time: a
+// panel it covers whole is stored at once; the partial first and last panels
+// of its range stay in registers until the end, go through LDS, and the wave
+// that holds a panel's first item adds the partials of the following waves
+// in wave order (no cross-workgroup traffic; deterministic).
+//
+// Per workgroup, LDS holds the activation scales and a table of every
+// block's offset in A_packed and precision, read once per batch.  With LDSA
+// the activation operand itself is unpacked to FP8 into LDS once per
+// workgroup (1 KB per 4-bit block, the hi and lo parts of an 8-bit block),
+// so an item's fragment is two LDS reads with no unpacking; otherwise each
+// item reads its fragment from L2 and unpacks it.
+constexpr int kStreamWaves = 16;
+constexpr int kSB = 4;  // items per batch
+
+struct StreamLayout {
+  int a_bytes;     // unpacked activation operand (LDSA), else 0
+  int sa_off;      // activation scales, fp16 [NG][8]
+  int info_off;    // block table, int [NG + kSB]
+  int bytes;       // total, at least the partials' [waves][2][64] f32x4
+};
+
+__host__ __device__ inline StreamLayout stream_layout(int NG, int n8, bool ldsa) {
+  StreamLayout l;
+  l.a_bytes = ldsa ? (NG + n8) * 1024 : 0;
+  l.sa_off = l.a_bytes;
+  l.info_off = l.sa_off + NG * 16;
+  const int end = l.info_off + (NG + kSB) * 4;
+  const int part = kStreamWaves * 2 * 64 * 16;
+  l.bytes = end > part ? end : part;
+  return l;
+}
+
+// Weight scales of the batch whose first item is block g of local panel q:
+// lane l holds the two fp16 scales of columns 2 (l % 8), 2 (l % 8) + 1 of
+// item l / 8 (panel clamped to qmax past the range; such items are never
+// computed).
+__device__ __forceinline__ uint32_t stream_sw(const GemmArgs& p, int pbase, int q, int g,
+                                              int qmax) {
+  const int lane = threadIdx.x & 63;
+  const int NG = p.K / kG;
+  int gi = g + (lane >> 3), qi = q;
+  if (gi >= NG) {
+    gi -= NG;
+    ++qi;
+  }
+  qi = min(qi, qmax);
+  return *reinterpret_cast<const uint32_t*>(p.sw + (size_t)gi * p.N + 16 * (pbase + qi) +
+                                            2 * (lane & 7));
+}
+
+// Weights of items it0 .. it0 + 3 (clamped to ilast): lane r + 16 q reads row
+// r's 16-byte chunk q of each item's kilobyte.
+__device__ __forceinline__ void stream_w(const uint8_t* wbase, int it0, int ilast,
+                                         u32x4 (&w)[kSB]) {
+  const int lane = threadIdx.x & 63;
+  const uint8_t* b = wbase + (lane & 15) * 64 + (lane >> 4) * 16;
+  #pragma unroll
+  for (int i = 0; i < kSB; ++i) {
+    const int it = min(it0 + i, ilast);
+    w[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(b + (size_t)it * 1024));
+  }
+}
+
+__device__ __forceinline__ void stream_store(const GemmArgs& p, int panel, const f32x4& C) {
+  const int lane = threadIdx.x & 63;
+  const int col = 16 * panel + (lane & 15);
+  #pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * (lane >> 4) + i;
+    if (row < p.M) p.out[(size_t)row * p.N + col] = __half_as_ushort(__float2half_rn(C[i]));
+  }
+}
+
+// Activation fragment of block g (offset aoff in units of M * 64 bytes) for
+// M <= 8 from L2: rows 8..15 of the operand are padding, so lane r of each
+// 16-lane row reads row r & 7: its first 16 bytes, or for an 8-bit block with
+// r >= 8 the second 16 bytes of the same 32-byte chunk (moved down eight
+// lanes at use).
+__device__ __forceinline__ u32x4 stream_a_l2(const GemmArgs& p, int aoff, bool b8) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const uint32_t ub8 = b8 ? 1u : 0u;
+  const uint32_t row = (uint32_t)min(r16 & 7, p.M - 1);
+  const uint32_t second = ((uint32_t)r16 >> 3) & ub8;
+  return *reinterpret_cast<const u32x4*>(p.A + (size_t)p.M * 64 * (size_t)aoff +
+                                         (row << (6 + ub8)) + ((uint32_t)q4 << (4 + ub8)) +
+                                         (second << 4));
+}
+
+// One item: the block sums y of weights wraw (16 columns) against block g's
+// activation fragment, from LDS (LDSA: unpacked at aoff KB) or from the L2
+// fragment xa; then the dequantization C += y * (sa sw), or (DIAG) the exact
+// sums of the window.
+template <bool LDSA, bool DIAG>
+__device__ __forceinline__ void stream_step(const GemmArgs& p, const uint8_t* sA,
+                                            const uint16_t* sSa, const u32x4& wraw,
+                                            const u32x4& xa, int g, int aoff, bool b8,
+                                            uint32_t swpair, int i, int n0, f32x4& C) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  u32x4 wlo, whi;
+  unpack4(wraw, wlo, whi);
+  const i32x8 wf = {(int)wlo[0], (int)wlo[1], (int)wlo[2], (int)wlo[3],
+                    (int)whi[0], (int)whi[1], (int)whi[2], (int)whi[3]};
+  f32x4 y;
+  if constexpr (LDSA) {
+    const uint8_t* fa = sA + (size_t)aoff * 1024 + (r16 & 7) * 128 + q4 * 32;
+    const u32x4 a0 = *reinterpret_cast<const u32x4*>(fa);
+    const u32x4 a1 = *reinterpret_cast<const u32x4*>(fa + 16);
+    const i32x8 af = {(int)a0[0], (int)a0[1], (int)a0[2], (int)a0[3],
+                      (int)a1[0], (int)a1[1], (int)a1[2], (int)a1[3]};
+    if (b8) {
+      const u32x4 l0 = *reinterpret_cast<const u32x4*>(fa + 1024);
+      const u32x4 l1 = *reinterpret_cast<const u32x4*>(fa + 1040);
+      const i32x8 al = {(int)l0[0], (int)l0[1], (int)l0[2], (int)l0[3],
+                        (int)l1[0], (int)l1[1], (int)l1[2], (int)l1[3]};
+      const f32x4 yh = mfma_fp8(af, wf, f32x4{0.f, 0.f, 0.f, 0.f});
+      y = mfma_fp8(al, wf, yh * 8.0f);  // exact: integers below 2^24 units
+    } else {
+      y = mfma_fp8(af, wf, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+  } else {
+    if (b8) {
+      i32x8 al, ah;
+      u32x4 x1;
+      #pragma unroll
+      for (int k = 0; k < 4; ++k)
+        x1[k] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)xa[k], 0x128, 0xF, 0xF, false);
+      #pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        al[k] = (int)lo8(xa[k]);
+        al[4 + k] = (int)lo8(x1[k]);
+        ah[k] = (int)hi8(xa[k]);
+        ah[4 + k] = (int)hi8(x1[k]);
+      }
+      const f32x4 yh = mfma_fp8(ah, wf, f32x4{0.f, 0.f, 0.f, 0.f});
+      y = mfma_fp8(al, wf, yh * 8.0f);
+    } else {
+      u32x4 alo, ahi;
+      unpack4(xa, alo, ahi);
+      const i32x8 af = {(int)alo[0], (int)alo[1], (int)alo[2], (int)alo[3],
+                        (int)ahi[0], (int)ahi[1], (int)ahi[2], (int)ahi[3]};
+      y = mfma_fp8(af, wf, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+  }
+  if constexpr (DIAG) {
+    const int NG = p.K / kG;
+    const int col = n0 + r16;
+    #pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 4 * q4 + k;
+      if (row >= p.win_m0 && row < p.win_m1 && col >= p.win_n0 && col < p.win_n1) {
+        const size_t idx = ((size_t)(row - p.win_m0) * (p.win_n1 - p.win_n0) +
+                            (col - p.win_n0)) * NG + g;
+        p.acc[idx] = (int32_t)(y[k] * kUnit);
+      }
+    }
+  } else {
+    // 4x4x1 operands: activation scale of row 4 q4 + (lane & 3), weight scale
+    // of column lane % 16 (lane 8 i + c / 2 holds it, half c % 2)
+    const uint32_t swb = (uint32_t)__shfl((int)swpair, 8 * i + (r16 >> 1)) >> (16 * (r16 & 1));
+    const float sa =
+        __half2float(__ushort_as_half(sSa[g * 8 + min(4 * q4 + (lane & 3), p.M - 1)])) * kUnit;
+    const float sw = __half2float(__ushort_as_half((unsigned short)swb));
+    const f32x4 P = scale_products(sa, sw);
+    #pragma unroll
+    for (int k = 0; k < 4; ++k) C[k] = __builtin_fmaf(y[k], P[k], C[k]);
+  }
+}
+
+template <bool LDSA, bool DIAG>
+__global__ __launch_bounds__(kStreamWaves * 64) void skinny_stream_kernel(GemmArgs p, int kp,
+                                                                          StreamLayout lay) {
+  constexpr int NW = kStreamWaves;
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int NG = p.K / kG;
+  const int items = kp * NG;
+  const int pbase = blockIdx.x * kp;  // first panel of the workgroup
+  const uint8_t* wbase = p.W + (size_t)pbase * NG * 1024;
+  // this wave's items [i0, i1) (local indices) and its first and last panels
+  const int i0 = items * wave / NW, i1 = items * (wave + 1) / NW;
+  const int q0 = i0 / NG, q1 = (i1 - 1) / NG;
+  uint8_t* sA = smem;
+  uint16_t* sSa = reinterpret_cast<uint16_t*>(smem + lay.sa_off);
+  int* sInfo = reinterpret_cast<int*>(smem + lay.info_off);
+
+  // (panel, block) of the next batch to load, wave-uniform
+  int lq = q0, lg = i0 - q0 * NG;
+  auto advance = [&]() {
+    lg += kSB;
+    if (lg >= NG) {
+      lg -= NG;
+      ++lq;
+    }
+  };
+  u32x4 wa[kSB], wb[kSB];
+  uint32_t swa = 0, swb = 0;
+  if (i0 < i1) {
+    stream_w(wbase, i0, i1 - 1, wa);
+    swa = stream_sw(p, pbase, lq, lg, kp - 1);
+    advance();
+  }
+  // per workgroup: activation scales, block table (four entries past the end
+  // wrap to blocks 0..3), and with LDSA the unpacked activation operand: for
+  // every block and row r < 8 (clamped to M - 1) 128 FP8 bytes at aoff KB +
+  // 128 r, an 8-bit block's lo parts one KB after its hi parts
+  for (int e = threadIdx.x; e < NG * 8; e += NW * 64)
+    sSa[e] = p.sa[(size_t)(e >> 3) * p.M + min(e & 7, p.M - 1)];
+  for (int e = threadIdx.x; e < NG + kSB; e += NW * 64) {
+    const int gi = e < NG ? e : e - NG;
+    sInfo[e] = aoff_of(p, gi) | (is8(p, gi) ? 1 << 16 : 0);
+  }
+  if constexpr (LDSA) {
+    for (int e = threadIdx.x; e < NG * 64; e += NW * 64) {
+      const int gi = e >> 6, r = (e >> 3) & 7, c = e & 7;  // block, row, 16-code chunk
+      const int ao = aoff_of(p, gi);
+      const int row = min(r, p.M - 1);
+      uint8_t* dst = sA + (size_t)ao * 1024 + r * 128 + c * 16;
+      if (!is8(p, gi)) {
+        const uint2 v =
+            *reinterpret_cast<const uint2*>(p.A + (size_t)ao * p.M * 64 + row * 64 + c * 8);
+        *reinterpret_cast<u32x4*>(dst) =
+            u32x4{v.x & kSignMag, rotr4(v.x) & kSignMag, v.y & kSignMag, rotr4(v.y) & kSignMag};
+      } else {
+        const u32x4 v =
+            *reinterpret_cast<const u32x4*>(p.A + (size_t)ao * p.M * 64 + row * 128 + c * 16);
+        *reinterpret_cast<u32x4*>(dst) = u32x4{hi8(v[0]), hi8(v[1]), hi8(v[2]), hi8(v[3])};
+        *reinterpret_cast<u32x4*>(dst + 1024) = u32x4{lo8(v[0]), lo8(v[1]), lo8(v[2]), lo8(v[3])};
+      }
+    }
+  }
+  __syncthreads();
+
+  f32x4 C = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 F = C, L = C;  // partials of the first and last panel of the range
+  if (i0 < i1) {
+    int q = q0, g = i0 - q0 * NG;
+    // one batch of four items from weights wc / scales swc while the next
+    // batch loads into wn / swn
+    auto batch = [&](int ib, const u32x4 (&wc)[kSB], u32x4 (&wn)[kSB], uint32_t swc,
+                     uint32_t& swn) {
+      // this batch's block table entries (one LDS read, then scalars) and,
+      // from L2, its activation fragments
+      const int info = sInfo[g + (lane & (kSB - 1))];
+      u32x4 xa[kSB];
+      if constexpr (!LDSA) {
+        #pragma unroll
+        for (int i = 0; i < kSB; ++i) {
+          const int inf = __builtin_amdgcn_readlane(info, i);
+          xa[i] = stream_a_l2(p, inf & 0xFFFF, (inf >> 16) & 1);
+        }
+      }
+      stream_w(wbase, ib + kSB, i1 - 1, wn);
+      swn = stream_sw(p, pbase, lq, lg, kp - 1);
+      advance();
+      issue_point();
+      #pragma unroll
+      for (int i = 0; i < kSB; ++i) {
+        const int it = ib + i;
+        const int inf = __builtin_amdgcn_readlane(info, i);
+        if (it < i1) {
+          stream_step<LDSA, DIAG>(p, sA, sSa, wc[i], xa[LDSA ? 0 : i], g, inf & 0xFFFF,
+                                  (inf >> 16) & 1, swc, i, 16 * (pbase + q), C);
+          const bool last = g + 1 == NG;
+          g = last ? 0 : g + 1;
+          if (last || it + 1 == i1) {
+            // end of a panel or of the range
+            if constexpr (!DIAG) {
+              if (q * NG >= i0 && (q + 1) * NG <= i1)
+                stream_store(p, pbase + q, C);
+              else if (q == q0)
+                F = C;
+              else
+                L = C;
+            }
+            C = f32x4{0.f, 0.f, 0.f, 0.f};
+            ++q;
+          }
+        }
+      }
+    };
+    for (int ib = i0;;) {
+      batch(ib, wa, wb, swa, swb);
+      ib += kSB;
+      if (ib >= i1) break;
+      batch(ib, wb, wa, swb, swa);
+      ib += kSB;
+      if (ib >= i1) break;
+    }
+  }
+  if constexpr (DIAG) return;
+  // partials through LDS (the activation copy is no longer needed)
+  __syncthreads();
+  f32x4* part = reinterpret_cast<f32x4*>(smem);  // [NW][2][64]
+  part[(wave * 2 + 0) * 64 + lane] = F;
+  part[(wave * 2 + 1) * 64 + lane] = L;
+  __syncthreads();
+  for (int q = q0; q <= q1 && i0 < i1; ++q) {
+    const int first = q * NG, end = (q + 1) * NG;
+    if (first < i0 || end <= i1) continue;  // started by an earlier wave, or complete here
+    f32x4 acc = part[(wave * 2 + (q == q0 ? 0 : 1)) * 64 + lane];
+    for (int w = wave + 1; w < NW; ++w) {
+      const int j0 = items * w / NW, j1 = items * (w + 1) / NW;
+      if (j0 >= end) break;
+      if (j1 > j0) acc += part[(w * 2) * 64 + lane];
+    }
+    stream_store(p, pbase + q, acc);
+  }
+}
+
+template <bool LDSA, bool DIAG>
+const void* stream_fn() {
+  return reinterpret_cast<const void*>(&skinny_stream_kernel<LDSA, DIAG>);
+}
+
+int map_n8(const BlockMap& m) {
+  int n = 0;
+  for (int w = 0; w < kMaxBlocks / 64; ++w) n += __builtin_popcountll(m.bits[w]);
+  return n;
+}
+
 }  // namespace
 
+bool skinny_stream_eligible(int M, int N, int K, int cus) {
+  const int P = N / 16, NG = K / kG;
+  return M <= 8 && cus > 0 && P % cus == 0 && (P / cus) * NG >= kStreamWaves * 2 * kSB;
+}
+
+hipError_t set_skinny_attributes() {
+  const void* fns[4] = {stream_fn<true, false>(), stream_fn<true, true>(), stream_fn<false, false>(),
+                        stream_fn<false, true>()};
+  for (const void* f : fns) {
+    hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kStreamMaxLds);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream) {
+  if (skinny_stream_eligible(a.M, a.N, a.K, a.cus)) {
+    const int NG = a.K / kG, kp = a.N / 16 / a.cus;
+    // the unpacked operand in LDS pays when it fits and a workgroup has
+    // enough items to amortise unpacking it
+    StreamLayout lay = stream_layout(NG, map_n8(a.map), true);
+    const bool ldsa = lay.bytes <= kStreamMaxLds && kp * NG >= 512;
+    if (!ldsa) lay = stream_layout(NG, 0, false);
+    const dim3 grid(a.cus), block(kStreamWaves * 64);
+    if (ldsa) {
+      if (diag)
+        hipLaunchKernelGGL((skinny_stream_kernel<true, true>), grid, block, lay.bytes, stream, a, kp, lay);
+      else
+        hipLaunchKernelGGL((skinny_stream_kernel<true, false>), grid, block, lay.bytes, stream, a, kp, lay);
+    } else {
+      if (diag)
+        hipLaunchKernelGGL((skinny_stream_kernel<false, true>), grid, block, lay.bytes, stream, a, kp, lay);
+      else
+        hipLaunchKernelGGL((skinny_stream_kernel<false, false>), grid, block, lay.bytes, stream, a, kp, lay);
+    }
+    return hipGetLastError();
+  }
+
   if (a.splits < 1 || kWaves % a.splits != 0) return hipErrorInvalidValue;
   // 8 < M <= 32: the shared-activation kernel.  At M <= 8 the per-wave kernel
   // is faster: it needs fewer registers (four waves per SIMD against three),

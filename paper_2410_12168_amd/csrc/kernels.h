@@ -43,6 +43,7 @@ struct GemmArgs {
   const int* split_index;  // tile -> index into the partial/counter arrays (-1: not split)
   int M, N, K;
   int tiles_n;        // tiles along N
+  int cus;            // compute units of the device
   int splits;         // split-K slots per column block (few-token kernel)
   int win_m0, win_m1, win_n0, win_n1;
   BlockMap map;
@@ -89,12 +90,18 @@ hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, b
 // and FMPQ quantization of h [M][I] with `map` into A / sa [I/G][M].
 hipError_t launch_swiglu_quantize(const uint16_t* GU, uint8_t* A, uint16_t* sa, int M, int I,
                                   const BlockMap& map, hipStream_t stream);
-// Few-token kernels (M <= kSkinnyMaxM): one wave per (16 columns, split-K
+// Few-token kernels (M <= kSkinnyMaxM): for M <= 8, when the 16-column
+// panels divide evenly over the CUs, a persistent kernel whose waves stream
+// contiguous runs of W_packed; otherwise one wave per (16 columns, split-K
 // slot), or, for 8 < M <= 32 with at most two slots, four column blocks per
 // workgroup sharing the activation operand through LDS.
 constexpr int kSkinnyMaxM = 48;
+constexpr int kStreamMaxLds = 160 * 1024;
+bool skinny_stream_eligible(int M, int N, int K, int cus);
 inline bool skinny_shared(int M, int splits) { return M > 8 && M <= 32 && splits <= 2; }
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream);
+// Allows the stream kernels' dynamic LDS size; once per process and device.
+hipError_t set_skinny_attributes();
 // Split-K slots (1, 2 or 4) for the few-token kernel: spread the (N/16 x
 // slots) waves evenly over the device's SIMDs, keeping at least 4 K-blocks per
 // slot.

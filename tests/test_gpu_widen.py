@@ -175,3 +175,33 @@ def test_schedule_modes_agree(M, N, K, placement):
             assert_out_close(host_u16(out).view(np.float16)[rows], ref, f"mode {mode}")
     finally:
         os.environ.pop("COMET_SCHED", None)
+
+
+STREAM = [
+    # (M, N, K, map kind): the persistent few-token stream kernel runs when
+    # the 16-column panels divide evenly over the CUs (256 here)
+    (1, 57344, 8192, "cfg0"),      # 70B gate_up: activations unpacked in LDS, 56 items per wave
+    (8, 57344, 8192, "random"),
+    (3, 8192, 8192, "alternate"),  # 70B o: activations from L2, 8 waves per panel
+    (8, 8192, 28672, "cfg0"),      # 70B down: activations from L2 (too large for LDS)
+    (5, 98304, 768, "random"),     # 1.5 panels per wave: complete and partial panels mixed
+    (2, 65536, 1024, "all8"),      # one complete panel per wave
+]
+
+
+@pytest.mark.parametrize("M,N,K,kind", STREAM)
+def test_stream_kernel_matches_oracle(M, N, K, kind):
+    from test_gpu_parity import make_map
+
+    NG = K // 128
+    prec = make_map(kind, NG, seed=N)
+    win = (0, M, N // 2 - 24, N // 2 + 40)
+    print(f"stream kernel M={M} N={N} K={K} {kind}", flush=True)
+    r = run_path(M, N, K, prec, seed=M + K, diag_window=win)
+    qa, sa = oracle.quantize_act(r["X16"], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    assert np.array_equal(host(r["acc"]), oracle.group_acc(qa, qw[win[2]:win[3]]))
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"stream {M}x{N}x{K}")
+    again = comet.w4ax_gemm(r["A"], prec, r["sa"], r["Wp"], r["sw"], M, N, K)
+    assert torch.equal(r["out"].view(torch.int16), again.view(torch.int16))
