@@ -255,8 +255,12 @@ COMET_API comet_status_t comet_w4ax_gemm_noalloc(const uint8_t* A_packed,
  * A channel permutation for the down projection needs no runtime step here:
  * permute the gate and up rows (and the down projection's weight columns,
  * comet_pack_w4_perm) offline.  Other arguments and errors as comet_w4ax_gemm;
- * M at most 2,097,120.  For M <= 48 the GEMM writes fp16 to a library-owned
- * workspace (per device and stream) that comet_swiglu_quantize then reads. */
+ * M at most 2,097,120.  The epilogue fusion runs with the 128-row tile kernel
+ * (comet_gemm_kernel() == COMET_KERNEL_MID); with the other kernels the GEMM
+ * writes its fp16 output to a library-owned workspace (M * N * 2 bytes, per
+ * device and stream, kept until comet_release_caches) that the SwiGLU
+ * quantizer of comet_swiglu_quantize then reads, because that pair is faster
+ * there. */
 COMET_API comet_status_t comet_w4ax_gemm_swiglu_quant(
     const uint8_t* A_packed, const uint8_t* group_prec_map, const uint16_t* a_scales,
     const uint8_t* W_packed, const uint16_t* w_scales, int M, int N, int K, int G,

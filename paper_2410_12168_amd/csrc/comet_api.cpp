@@ -410,11 +410,22 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   a.win_n0 = n0;
   a.win_n1 = n1;
   a.map = map;
-  if (swiglu && skinny) {
+  // The SwiGLU epilogue is fused into the 128-row tile kernel only.  With
+  // the few-token kernels and the 256-row tile kernel, the GEMM plus the
+  // standalone SwiGLU quantizer is faster (the epilogue's exp and division
+  // then run on the whole chip at once, not on one tile's waves after its
+  // K-loop), so the GEMM writes fp16 to the stream's workspace first.
+  if (swiglu && kind != COMET_KERNEL_MID) {
     uint16_t* tmp;
     if ((st = get_tmp(dev, stream, (size_t)M * N * sizeof(uint16_t), &tmp))) return st;
     a.out = tmp;
-    if ((st = launched(comet::launch_gemm_skinny(a, false, stream), "gemm launch"))) return st;
+    if (skinny)
+      st = launched(comet::launch_gemm_skinny(a, false, stream), "gemm launch");
+    else
+      st = launched(comet::launch_gemm(a, plan->host.num_wgs, false, false, mode == "natural",
+                                       plan->host.tile_m, stream),
+                    "gemm launch");
+    if (st) return st;
     return launched(comet::launch_swiglu_quantize(tmp, swiglu->A, swiglu->sa, M, N / 2,
                                                   swiglu->map, stream),
                     "swiglu_quantize launch");

@@ -4,24 +4,26 @@
 //
 // A lane holds 8 consecutive channels of one (row, block) pair and 16 lanes
 // hold the block.  Scale and codes follow the block quantizer exactly:
-// s = fp16_rne(fp32(amax / qmax)) by one IEEE division, then per element
-// q = clamp(rint(RN(x / s)), -qmax, qmax), packed sign-magnitude.
+// s = fp16_rne(RN(amax / qmax)), then per element
+// q = clamp(rint(RN(x / s)), -qmax, qmax), packed sign-magnitude; every
+// division is the correctly rounded quotient, computed as below.
 //
 // Division.  The codes need RN(x / s) exactly (IEEE fp32 division), which as
 // a library division costs about ten vector instructions per element and made
-// these kernels ALU-bound.  Instead each lane takes one correctly rounded
-// reciprocal r = RN(1/s) and per element
+// these kernels ALU-bound.  Instead each lane takes one reciprocal r within
+// one ulp of 1/s (RN(1/s), or the hardware reciprocal) and per element
 //     q0 = RN(x r),  rem = x - q0 s  (one fma, exact),  q = RN(q0 + rem r),
 // Markstein's correction step.  Why q = RN(x / s) here: s is a binary16
 // value, so its significand has at most 11 bits.  q0 is within 2 ulps of x/s,
 // so rem is a multiple of ulp(q0) * 2^e(s) of at most 13 bits: exact.  The
-// fma then sees x/s perturbed by at most |rem| |r - 1/s| <= 2^-46 ulp-units
+// fma then sees x/s perturbed by at most |rem| |r - 1/s| <= 2^-45 ulp-units
 // of the result, while x/s, when it is not a midpoint between binary32
 // neighbours, lies at least 2^-35 units from one (x has 24 bits, s 11 bits),
 // and it is never exactly a midpoint (a midpoint needs 25 significant bits
 // times s's odd part).  So rounding the perturbed value gives RN(x / s).  The
-// identity is also checked exhaustively over every binary16 operand pair on
-// the CPU.  s == 0 takes r = 0, which yields q = 0 as the quantizer requires.
+// identity is also checked exhaustively on the CPU, over every binary16
+// operand pair and with r = RN(1/s) and both of its neighbours.  s == 0 takes
+// r = 0, which yields q = 0 as the quantizer requires.
 //
 #pragma once
 
@@ -48,12 +50,18 @@ __device__ inline float div_rn(float a, float s, float r) {
 
 // Magnitudes and signs follow q = clamp(rint(x / s), -qmax, qmax) with the
 // sign taken from x (rint and the division are symmetric); a zero code has a
-// clear sign bit.
+// clear sign bit.  Both divisions go through div_rn: the scale RN(amax / qmax)
+// with the constant RN(1/qmax), the codes with r from the hardware
+// reciprocal.  div_rn needs r within one ulp of 1/s, not correctly rounded
+// (the margin argument above has room to spare); v_rcp_f32 is within one ulp,
+// and both neighbours of RN(1/s) are checked exhaustively on the CPU, as is
+// every amax / qmax.
 __device__ inline uint16_t quantize8(const float (&x)[8], float amax, float qmax, Codes& c) {
-  float s32 = amax / qmax;
+  const float rq = qmax == 127.0f ? 1.0f / 127.0f : 1.0f / 7.0f;  // folded: RN(1/qmax)
+  float s32 = div_rn(amax, qmax, rq);
   __half h = __float2half_rn(s32);
   float s = __half2float(h);
-  const float r = s != 0.0f ? 1.0f / s : 0.0f;
+  const float r = s != 0.0f ? __builtin_amdgcn_rcpf(s) : 0.0f;
   #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const float m = fminf(rintf(div_rn(fabsf(x[i]), s, r)), qmax);
@@ -96,12 +104,18 @@ __device__ inline void load8(const uint16_t* p, float (&x)[8]) {
   }
 }
 
+// v from the lane that the DPP control selects within its 16-lane row
+#define COMET_DPP_F32(v, ctrl) \
+  __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xF, 0xF, false))
+
 __device__ inline float max16(float v) {
-  // butterfly over the 16 lanes of one (row, block) pair
-  v = fmaxf(v, __shfl_xor(v, 1, 16));
-  v = fmaxf(v, __shfl_xor(v, 2, 16));
-  v = fmaxf(v, __shfl_xor(v, 4, 16));
-  v = fmaxf(v, __shfl_xor(v, 8, 16));
+  // max over the 16 lanes of one (row, block) pair, within the DPP row: the
+  // quad butterflies (quad_perm [1,0,3,2] and [2,3,0,1]) give every lane its
+  // quad's max, rotating the row by 4 and then 8 lanes combines the four quads
+  v = fmaxf(v, COMET_DPP_F32(v, 0xB1));
+  v = fmaxf(v, COMET_DPP_F32(v, 0x4E));
+  v = fmaxf(v, COMET_DPP_F32(v, 0x124));
+  v = fmaxf(v, COMET_DPP_F32(v, 0x128));
   return v;
 }
 

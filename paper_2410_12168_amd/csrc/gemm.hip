@@ -951,8 +951,9 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
 
 typedef void (*GemmKernelFn)(GemmArgs);
 
-// The instantiations: production (plain, diagnostic, SwiGLU epilogue) and the
-// natural-order ablation (plain, diagnostic), for both tile heights.
+// The instantiations: production (plain, diagnostic; the SwiGLU epilogue for
+// the 128-row kernel only) and the natural-order ablation (plain,
+// diagnostic), for both tile heights.  nullptr: not instantiated.
 GemmKernelFn gemm_kernel_fn(int tile_m, bool diag, bool swiglu, bool natural) {
   if (tile_m == kMidTM) {
     if (natural) return diag ? gemm_mid_kernel<true, false, true> : gemm_mid_kernel<false, false, true>;
@@ -960,8 +961,8 @@ GemmKernelFn gemm_kernel_fn(int tile_m, bool diag, bool swiglu, bool natural) {
     return swiglu ? gemm_mid_kernel<false, true, false> : gemm_mid_kernel<false, false, false>;
   }
   if (natural) return diag ? gemm_kernel<256, true, false, true> : gemm_kernel<256, false, false, true>;
-  if (diag) return gemm_kernel<256, true, false, false>;
-  return swiglu ? gemm_kernel<256, false, true, false> : gemm_kernel<256, false, false, false>;
+  if (swiglu) return nullptr;  // the 256-row kernel's SwiGLU runs as its own kernel
+  return diag ? gemm_kernel<256, true, false, false> : gemm_kernel<256, false, false, false>;
 }
 
 }  // namespace
@@ -971,9 +972,10 @@ int gemm_lds_bytes(int tile_m) { return tile_m == kMidTM ? kMidLds : Geo<256>::L
 hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, bool natural,
                        int tile_m, hipStream_t stream) {
   const dim3 grid(num_wgs), block(kThreads);
-  if (swiglu && natural) return hipErrorInvalidValue;  // not instantiated
+  const GemmKernelFn fn = swiglu && natural ? nullptr : gemm_kernel_fn(tile_m, diag, swiglu, natural);
+  if (!fn) return hipErrorInvalidValue;  // not instantiated
   const int lds = tile_m == kMidTM ? kMidLds : Geo<256>::Lds;
-  hipLaunchKernelGGL(gemm_kernel_fn(tile_m, diag, swiglu, natural), grid, block, lds, stream, a);
+  hipLaunchKernelGGL(fn, grid, block, lds, stream, a);
   return hipGetLastError();
 }
 
@@ -981,9 +983,11 @@ hipError_t set_gemm_attributes() {
   for (int tm : {256, kMidTM})
     for (int v = 0; v < 5; ++v) {
       const bool diag = v == 1 || v == 4, swiglu = v == 2, natural = v >= 3;
-      hipError_t e = hipFuncSetAttribute(
-          reinterpret_cast<const void*>(gemm_kernel_fn(tm, diag, swiglu, natural)),
-          hipFuncAttributeMaxDynamicSharedMemorySize, tm == kMidTM ? kMidLds : Geo<256>::Lds);
+      const GemmKernelFn fn = gemm_kernel_fn(tm, diag, swiglu, natural);
+      if (!fn) continue;
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         tm == kMidTM ? kMidLds : Geo<256>::Lds);
       if (e != hipSuccess) return e;
     }
   return hipSuccess;

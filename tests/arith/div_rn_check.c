@@ -10,6 +10,11 @@
  *   seeded random binary16 pairs x >= mn with (x - mn) <= 16 * s, plus every
  *   binary32 value within 64 ulps of each midpoint (k + 1/2) * s, k = 0..15
  *   (the KV4 quantizer: a = x - mn <= 15 * s * (1 + 2^-10)).
+ * mode "qmax": s in {7, 127} (the block quantizers' scale s = RN(amax / qmax)),
+ *   a over every non-negative finite binary16 value, r = RN(1/s).
+ * With a second argument "nbr" (modes fp16 and kv), r also takes the two
+ *   binary32 neighbours of RN(1/s): every result within one ulp of 1/s (what a
+ *   hardware reciprocal guarantees) is covered.
  * Prints the number of pairs checked and of mismatches; exit status 1 on any
  * mismatch.  Built with -ffp-contract=off so a * r is a plain multiply. */
 #include <math.h>
@@ -43,12 +48,20 @@ static float from_bits(uint32_t u) {
 
 static volatile float sink;
 
-static int check(float a, float s, float r) {
+static int check1(float a, float s, float r) {
   float q0 = a * r;
   float rem = fmaf(-q0, s, a);
   float q = fmaf(rem, r, q0);
   float want = a / s;
   return bits(q) != bits(want);
+}
+
+static int nbr = 0;
+
+static int check(float a, float s, float r) {
+  int bad = check1(a, s, r);
+  if (nbr) bad |= check1(a, s, nextafterf(r, 0.0f)) | check1(a, s, nextafterf(r, INFINITY));
+  return bad;
 }
 
 static uint64_t rng_state = 0x9E3779B97F4A7C15ull;
@@ -61,7 +74,20 @@ static uint64_t next64(void) {
 
 int main(int argc, char** argv) {
   const char* mode = argc > 1 ? argv[1] : "fp16";
+  nbr = argc > 2 && !strcmp(argv[2], "nbr");
   unsigned long long n = 0, bad = 0;
+  if (!strcmp(mode, "qmax")) {
+    const float qs[2] = {7.0f, 127.0f};
+    for (int i = 0; i < 2; ++i) {
+      const float s = qs[i], r = 1.0f / s;
+      for (uint32_t xh = 0; xh < 0x7C00; ++xh) {
+        ++n;
+        bad += check1(f16((uint16_t)xh), s, r);
+      }
+    }
+    printf("%s: %llu pairs, %llu mismatches\n", mode, n, bad);
+    return bad ? 1 : 0;
+  }
   for (uint32_t sh = 1; sh < 0x7C00; ++sh) {
     float s = f16((uint16_t)sh);
     float r = 1.0f / s;

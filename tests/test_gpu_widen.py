@@ -205,3 +205,25 @@ def test_stream_kernel_matches_oracle(M, N, K, kind):
     assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"stream {M}x{N}x{K}")
     again = comet.w4ax_gemm(r["A"], prec, r["sa"], r["Wp"], r["sw"], M, N, K)
     assert torch.equal(r["out"].view(torch.int16), again.view(torch.int16))
+
+
+def test_quantizer_every_fp16_block_max():
+    """Every positive finite fp16 value as a block's max |x|, in a 4-bit and
+    an 8-bit block, with the other channels random fractions of it and exact
+    ties: every scale the quantizers can produce meets the hardware
+    reciprocal; codes and scales must equal the oracle's bit for bit."""
+    amax = np.arange(1, 0x7C00, dtype=np.uint16).view(np.float16).astype(np.float32)
+    M, K = amax.size, 256
+    rng = np.random.default_rng(0)
+    X = (rng.uniform(-1.0, 1.0, (M, K)).astype(np.float32) * amax[:, None])
+    X[:, 0] = amax
+    X[:, 128] = -amax
+    X[:, 1] = amax * (2.5 / 7.0)      # near code midpoints of the 4-bit block
+    X[:, 129] = amax * (64.5 / 127.0)  # and of the 8-bit block
+    X16 = X.astype(np.float16).view(np.uint16)
+    prec = np.array([4, 8], np.uint8)
+    print(f"every fp16 block max: M={M}", flush=True)
+    A, sa = comet.quantize_act(dev_u16(X16), prec)
+    qa, osa = oracle.quantize_act(X16, prec)
+    assert np.array_equal(host_u16(sa), osa)
+    assert np.array_equal(host(A), oracle.pack_act(qa, prec))
