@@ -59,6 +59,7 @@ KERNEL_SOURCES = {
     "skinny": ["gemm_skinny.hip", "operand.h", "kernels.h"],
     "skinny_shared": ["gemm_skinny.hip", "operand.h", "kernels.h"],
     "mid": ["gemm.hip", "operand.h", "kernels.h"],
+    "stream": ["gemm_skinny.hip", "operand.h", "kernels.h"],
     "kv4": ["kv4.hip"],
 }
 def gemm_kind(M: int, N: int, K: int, cus: int) -> str:

@@ -338,7 +338,7 @@ def comet_gemm_kernel(M: int, N: int, K: int, num_cus: int, G: int = G) -> int:
     return k
 
 
-KERNEL_NAMES = {0: "skinny", 1: "skinny_shared", 2: "mid", 3: "tile"}
+KERNEL_NAMES = {0: "skinny", 1: "skinny_shared", 2: "mid", 3: "tile", 4: "stream"}
 
 
 def comet_build_stamp() -> str:

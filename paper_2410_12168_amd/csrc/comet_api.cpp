@@ -171,11 +171,14 @@ std::string sched_mode() {
   return (m && *m) ? std::string(m) : std::string("cost");
 }
 
-// Which GEMM kernel runs for this shape on `cus` compute units.  The
-// few-token kernels take M <= 48, except that above 32 rows the 128-row tile
-// kernel takes over when its 256-column tiles cover at least 3/4 of the CUs
-// (wide N); the 128-row tile kernel runs up to M = 128, the 256-row one above.
+// Which GEMM kernel runs for this shape on `cus` compute units.  The stream
+// kernels take M <= 64 when the weight panels divide evenly over the CUs
+// (and each wave gets enough of them).  Otherwise the few-token kernels take
+// M <= 48, except that above 32 rows the 128-row tile kernel takes over when
+// its 256-column tiles cover at least 3/4 of the CUs (wide N); the 128-row
+// tile kernel runs up to M = 128, the 256-row one above.
 int kernel_kind(int M, int N, int K, int cus) {
+  if (comet::skinny_stream_eligible(M, N, K, cus)) return COMET_KERNEL_STREAM;
   const int col_tiles = (N + comet::kTileN - 1) / comet::kTileN;
   const bool wide = 4 * col_tiles >= 3 * cus;
   if (M <= comet::kSkinnyMaxM && !(M > kSkinnyWideM && wide))
@@ -366,7 +369,8 @@ comet_status_t run_gemm(const uint8_t* A, const uint8_t* prec, const uint16_t* s
   }
   const bool diag = acc != nullptr;
   const int kind = kernel_kind(M, N, K, info.cus);
-  const bool skinny = kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED;
+  const bool skinny = kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED ||
+                      kind == COMET_KERNEL_STREAM;
   // the few-token kernels walk the K-blocks in natural order and need no plan
   const DevicePlan* plan = nullptr;
   // the fused SwiGLU epilogue has no natural-order form: it takes "dp" instead
@@ -477,7 +481,8 @@ comet_status_t run_gemm_noalloc(const uint8_t* A, const uint8_t* prec, const uin
   a.cus = info.cus;
   a.map = map;
   for (int g = 0; g < K / comet::kG; ++g) a.n4 += prec[g] == 4;
-  if (kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED) {
+  if (kind == COMET_KERNEL_FEW_TOKEN || kind == COMET_KERNEL_FEW_TOKEN_SHARED ||
+      kind == COMET_KERNEL_STREAM) {
     a.splits = comet::skinny_splits(N, K, info.cus);
     return launched(comet::launch_gemm_skinny(a, false, stream), "gemm launch");
   }

@@ -172,6 +172,13 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :: "v"(g), "s"(lds) : "memory", "m0");
 }
+// The same with the non-temporal hint, for data used once (the mid-size
+// kernel's weights): it does not displace the activation codes, which every
+// workgroup reads, from L2.
+__device__ __forceinline__ void dma16nt(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt"
+               :: "v"(g), "s"(lds) : "memory", "m0");
+}
 
 // Source of one 1 KB wave load of packed weights: K-block g of the 16-column
 // panel j of the tile at n0 (one contiguous kilobyte of W_packed).  Lane L
@@ -749,7 +756,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 
 
 // ---------------------------------------------------------------------------
-// Mid-size GEMM (48 < M <= 128): 128-row tiles, with the workgroup's waves
+// Mid-size GEMM (up to 128 rows; see kernel_kind for where it runs): 128-row
+// tiles, with the workgroup's waves
 // split by role so that no load is waited for early.  With this few rows the
 // weights come from HBM exactly once and a K-block computes briefly, so the
 // loads need several K-blocks of lead, and a wait on the vector-memory counter
@@ -784,7 +792,7 @@ __device__ __forceinline__ void mid_dma(const GemmArgs& p, int g, int n0, uint32
   #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int j = 4 * wave + i;
-    dma16(w_src(p, g, n0, j), slot + j * 1024);
+    dma16nt(w_src(p, g, n0, j), slot + j * 1024);
   }
   const int c0 = min(n0 + 64 * wave + 8 * (lane & 7), p.N - 8);
   if (lane < 8) dma16(p.sw + (size_t)g * p.N + c0, slot + kWr + 128 * wave);

@@ -1,8 +1,14 @@
-// gemm_skinny.hip -- W4Ax GEMM for few tokens (decode, M <= 48) on gfx950.
+// gemm_skinny.hip -- W4Ax GEMM for few tokens (decode) on gfx950.
 //
-// With a handful of tokens the GEMM is a weight stream: every 4-bit weight is
-// read from HBM once and used by at most 48 activation rows, so the bound is
-// HBM bandwidth, not the matrix cores.  Each wave owns 16 output columns and
+// With a few tokens the GEMM is a weight stream: every 4-bit weight is read
+// from HBM once and used by few activation rows, so the bound is HBM
+// bandwidth, not the matrix cores.  Three designs live here:
+//   * the per-wave and shared-activation kernels (M <= 48, any N), first
+//     below;
+//   * the stream kernels (M <= 64, when the 16-column weight panels divide
+//     evenly over the CUs): each workgroup owns whole panels and streams them
+//     as contiguous runs, at the end of the file.
+// In the per-wave kernel each wave owns 16 output columns and
 // a contiguous K-block range (split-K slot), walked in natural block order in
 // batches of four K-blocks.  The wave's 16 weight rows are one panel of
 // W_packed, where each K-block is one contiguous kilobyte: one nontemporal
@@ -863,11 +869,417 @@ int map_n8(const BlockMap& m) {
   return n;
 }
 
+// ---------------------------------------------------------------------------
+// Chunked weight-stream kernel (8 < M <= 64).  As in the stream kernel above,
+// each workgroup owns kp whole 16-column panels (the panels divide evenly over
+// the CUs), so the weights leave HBM once, as long contiguous runs, and no
+// workgroup waits for another.  With more than eight rows the activation
+// operand of a whole row no longer fits in LDS, so the K-blocks are walked in
+// chunks of kChC: the workgroup's eight waves stage one chunk's activation
+// fragments (all R row blocks, 4-bit codes unpacked once) and scales in LDS
+// while computing the previous one, and one barrier per chunk publishes them.
+// The chunk's kp * kChC items (panel, K-block) are split evenly over the waves
+// in panel-major order, the same way in every chunk, so a wave always works on
+// the same (at most three) panels and keeps their accumulators in registers.
+// Each item's weights are one 16-byte load per lane, issued a chunk ahead;
+// per item the wave runs R MFMAs (2R for an 8-bit block) against the staged
+// fragments.  At the end, panels split between waves are added through LDS in
+// wave order (deterministic).
+constexpr int kChWaves = 8;
+constexpr int kChC = 4;                   // K-blocks per chunk
+constexpr int kChSeg = 3;                 // panels (segments) per wave
+constexpr int kChItems = 2 * kChC;        // most items per wave and chunk
+constexpr int kChMaxM = 64;               // rows (four row blocks)
+
+template <int R>
+struct ChLayout {
+  static constexpr int Frag = 2048;                   // one (K-block, row block): 64 lanes x 32 B
+  static constexpr int Stage = kChC * R * Frag;       // a chunk's activation fragments
+  static constexpr int Scales = kChC * 16 * R * 4;    // its fp32 activation scales (x 2^18)
+  static constexpr int Buf = Stage + Scales;
+  static constexpr int Part = kChWaves * 2 * R * 64 * 16;  // partial panels at the end
+  static constexpr int Bytes = 2 * Buf > Part ? 2 * Buf : Part;
+  static constexpr int Sets = (kChC * R + kChWaves - 1) / kChWaves;  // fragment sets per wave
+};
+
+// One staged fragment set (K-block c of the chunk, row block r): this lane's
+// 32 bytes (row 16 r + lane % 16, codes 32 (lane / 16) .. + 31), as loaded.
+struct ChSet {
+  u32x4 v[2];
+  bool b8;
+};
+
+// Loads of fragment set f of chunk ch (clamped into range: sets past the
+// chunk's end re-read a valid set and are not stored).
+template <int R>
+__device__ __forceinline__ void ch_set_load(const GemmArgs& p, int ch, int f, ChSet& s) {
+  const int lane = threadIdx.x & 63;
+  const int NG = p.K / kG;
+  const int c = min(f / R, kChC - 1), r = f % R;
+  const int g = min(ch * kChC + c, NG - 1);
+  s.b8 = is8(p, g);
+  const uint32_t b8 = s.b8 ? 1u : 0u;
+  const uint32_t row = (uint32_t)min(16 * r + (lane & 15), p.M - 1);
+  const uint8_t* base = p.A + (size_t)p.M * 64 * (size_t)aoff_of(p, g) + (row << (6 + b8)) +
+                        ((uint32_t)(lane >> 4) << (4 + b8));
+  s.v[0] = *reinterpret_cast<const u32x4*>(base);
+  s.v[1] = *reinterpret_cast<const u32x4*>(base + (b8 << 4));
+}
+
+template <int R>
+__device__ __forceinline__ void ch_set_store(const ChSet& s, int f, uint8_t* stage) {
+  const int lane = threadIdx.x & 63;
+  u32x4 lo = s.v[0], hi = s.v[1];
+  if (!s.b8) unpack4(s.v[0], lo, hi);
+  uint8_t* dst = stage + f * ChLayout<R>::Frag + lane * 32;  // f = c * R + r
+  *reinterpret_cast<u32x4*>(dst) = lo;
+  *reinterpret_cast<u32x4*>(dst + 16) = hi;
+}
+
+// Activation scales of chunk ch: entry c * 16 R + row, fp16 loaded here,
+// stored as fp32 times 2^18.  Thread t handles entries t and t + 512.
+template <int R>
+struct ChScales {
+  uint32_t v[(kChC * 16 * R + kChWaves * 64 - 1) / (kChWaves * 64)];
+};
+template <int R>
+__device__ __forceinline__ void ch_scales_load(const GemmArgs& p, int ch, ChScales<R>& s) {
+  const int NG = p.K / kG;
+  #pragma unroll
+  for (int i = 0; i < (int)(sizeof(s.v) / sizeof(s.v[0])); ++i) {
+    const int e = min((int)threadIdx.x + i * kChWaves * 64, kChC * 16 * R - 1);
+    const int c = e / (16 * R), row = e % (16 * R);
+    const int g = min(ch * kChC + c, NG - 1);
+    s.v[i] = p.sa[(size_t)g * p.M + min(row, p.M - 1)];
+  }
+}
+template <int R>
+__device__ __forceinline__ void ch_scales_store(const ChScales<R>& s, float* dst) {
+  #pragma unroll
+  for (int i = 0; i < (int)(sizeof(s.v) / sizeof(s.v[0])); ++i) {
+    const int e = (int)threadIdx.x + i * kChWaves * 64;
+    if (e < kChC * 16 * R) dst[e] = __half2float(__ushort_as_half((unsigned short)s.v[i])) * kUnit;
+  }
+}
+
+// Weights and weight scales of this wave's item k of chunk ch: item t = tb +
+// k (clamped below te: a slot past the wave's items re-reads its last item,
+// which costs no extra HBM traffic), panel pbase + t / kChC, K-block ch *
+// kChC + t % kChC clamped below NG.
+struct ChW {
+  u32x4 w;
+  uint32_t sw;
+};
+__device__ __forceinline__ void ch_w_load(const GemmArgs& p, int pbase, int tb, int te, int k,
+                                          int ch, ChW& x) {
+  const int lane = threadIdx.x & 63;
+  const int NG = p.K / kG;
+  // wave-uniform item, kept in scalar registers: each load is a scalar base
+  // plus the lane's constant offset
+  const int t = __builtin_amdgcn_readfirstlane(min(tb + k, te - 1));
+  const int g = min(ch * kChC + t % kChC, NG - 1);
+  const int panel = pbase + t / kChC;
+  const uint8_t* wb = p.W + ((size_t)panel * NG + g) * 1024;
+  const uint16_t* sb = p.sw + (size_t)g * p.N + 16 * panel;
+  x.w = __builtin_nontemporal_load(
+      reinterpret_cast<const u32x4*>(wb + (uint32_t)((lane & 15) * 64 + (lane >> 4) * 16)));
+  x.sw = sb[lane & 15];
+}
+
+// The wave's items at position c of the chunk (K-block g): with at most
+// 2 kChC items per wave, two slots kA and kA + kChC (segments sA and sA + 1),
+// the second computed only with TWO.  Each staged activation fragment (and
+// scale vector) is read once for both items.
+template <int R, bool DIAG, bool TWO>
+__device__ __forceinline__ void ch_group(const GemmArgs& p, const ChW& xa, const ChW& xb, int g,
+                                         int c, int n0a, const uint8_t* sA, const float* sS,
+                                         f32x4 (&Ca)[R], f32x4 (&Cb)[R]) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const int NG = p.K / kG;
+  const bool b8 = is8(p, g);
+  auto wfrag = [](const u32x4& w) {
+    u32x4 lo, hi;
+    unpack4(w, lo, hi);
+    return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                 (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+  };
+  const i32x8 wa = wfrag(xa.w);
+  i32x8 wb = wa;
+  if constexpr (TWO) wb = wfrag(xb.w);
+  const float swa = __half2float(__ushort_as_half((unsigned short)xa.sw));
+  const float swb = __half2float(__ushort_as_half((unsigned short)xb.sw));
+  // row block r + 1's fragment is read while row block r computes
+  const uint8_t* fr = sA + c * R * ChLayout<R>::Frag + lane * 32;
+  u32x4 n0v = *reinterpret_cast<const u32x4*>(fr), n1v = *reinterpret_cast<const u32x4*>(fr + 16);
+  #pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const u32x4 x0 = n0v, x1 = n1v;
+    if (r + 1 < R) {
+      n0v = *reinterpret_cast<const u32x4*>(fr + (r + 1) * ChLayout<R>::Frag);
+      n1v = *reinterpret_cast<const u32x4*>(fr + (r + 1) * ChLayout<R>::Frag + 16);
+    }
+    f32x4 ya, yb;
+    if (b8) {
+      i32x8 al, ah;
+      #pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        al[k] = (int)lo8(x0[k]);
+        al[4 + k] = (int)lo8(x1[k]);
+        ah[k] = (int)hi8(x0[k]);
+        ah[4 + k] = (int)hi8(x1[k]);
+      }
+      // exact: integers below 2^24 units
+      ya = mfma_fp8(al, wa, mfma_fp8(ah, wa, f32x4{0.f, 0.f, 0.f, 0.f}) * 8.0f);
+      if constexpr (TWO) yb = mfma_fp8(al, wb, mfma_fp8(ah, wb, f32x4{0.f, 0.f, 0.f, 0.f}) * 8.0f);
+    } else {
+      const i32x8 af = {(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3],
+                        (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};
+      ya = mfma_fp8(af, wa, f32x4{0.f, 0.f, 0.f, 0.f});
+      if constexpr (TWO) yb = mfma_fp8(af, wb, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+    if constexpr (DIAG) {
+      #pragma unroll
+      for (int h = 0; h < (TWO ? 2 : 1); ++h) {
+        const int col = n0a + 16 * h + r16;
+        const f32x4 y = h ? yb : ya;
+        #pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int row = 16 * r + 4 * q4 + k;
+          if (row >= p.win_m0 && row < p.win_m1 && col >= p.win_n0 && col < p.win_n1) {
+            const size_t idx = ((size_t)(row - p.win_m0) * (p.win_n1 - p.win_n0) +
+                                (col - p.win_n0)) * NG + g;
+            p.acc[idx] = (int32_t)(y[k] * kUnit);
+          }
+        }
+      }
+    } else {
+      const f32x4 sa4 = *reinterpret_cast<const f32x4*>(sS + c * 16 * R + 16 * r + 4 * q4);
+      const f32x4 Pa = sa4 * swa;  // exact: 11-bit by 11-bit significands
+      #pragma unroll
+      for (int k = 0; k < 4; ++k) Ca[r][k] = __builtin_fmaf(ya[k], Pa[k], Ca[r][k]);
+      if constexpr (TWO) {
+        const f32x4 Pb = sa4 * swb;
+        #pragma unroll
+        for (int k = 0; k < 4; ++k) Cb[r][k] = __builtin_fmaf(yb[k], Pb[k], Cb[r][k]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// The chunk loop for a wave whose first item sits at position A of its
+// panel's kChC K-blocks (A = tb % kChC): item k is then position (A + k) %
+// kChC of the wave's panel segment (A + k) / kChC, both known at compile time,
+// so the accumulators and weight registers are indexed statically.  Items
+// are computed by position (K-block) of the chunk, the two items at one
+// position together.
+template <int R, bool DIAG, int A>
+__device__ __forceinline__ void ch_run(const GemmArgs& p, uint8_t* smem, int pbase, int tb, int te,
+                                       f32x4 (&C)[kChSeg][R]) {
+  using L = ChLayout<R>;
+  static_assert(kChItems == 2 * kChC, "two items per chunk position");
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int NG = p.K / kG, NC = (NG + kChC - 1) / kChC;
+  const int n = te - tb;  // the wave's items per chunk
+  const int q0 = tb / kChC;
+  auto stage = [&](int ch) { return smem + (ch & 1) * L::Buf; };
+  auto scales = [&](int ch) { return reinterpret_cast<float*>(smem + (ch & 1) * L::Buf + L::Stage); };
+  constexpr int H = (L::Sets + 1) / 2;  // fragment sets staged per half chunk
+
+  // weight slot k holds item k; once a position's items are computed their
+  // slots load the same items of the next chunk
+  ChW w[kChItems];
+  #pragma unroll
+  for (int k = 0; k < kChItems; ++k) ch_w_load(p, pbase, tb, te, k, 0, w[k]);
+  for (int ch = 0; ch < NC; ++ch) {
+    const int cc = min(kChC, NG - ch * kChC);  // K-blocks in this chunk
+    const int chn = min(ch + 1, NC - 1);      // the chunk loaded ahead (the last re-reads itself)
+    const uint8_t* sA = stage(ch);
+    const float* sS = scales(ch);
+    ChSet st[H];
+    ChScales<R> ss;
+    #pragma unroll
+    for (int j = 0; j < H; ++j) ch_set_load<R>(p, chn, min(wave + kChWaves * j, kChC * R - 1), st[j]);
+    ch_scales_load<R>(p, chn, ss);
+    issue_point();
+    #pragma unroll
+    for (int c = 0; c < kChC; ++c) {
+      const int ka = (c - A + kChC) % kChC, kb = ka + kChC;  // the position's two slots
+      const int sa = (A + ka) / kChC;                        // segment of slot ka
+      const ChW xa = w[ka], xb = w[kb];
+      ch_w_load(p, pbase, tb, te, ka, chn, w[ka]);
+      ch_w_load(p, pbase, tb, te, kb, chn, w[kb]);
+      if (c < cc && ka < n) {
+        const int g = ch * kChC + c, n0a = 16 * (pbase + q0 + sa);
+        if (kb < n)
+          ch_group<R, DIAG, true>(p, xa, xb, g, c, n0a, sA, sS, C[sa], C[sa + 1 < kChSeg ? sa + 1 : sa]);
+        else
+          ch_group<R, DIAG, false>(p, xa, xb, g, c, n0a, sA, sS, C[sa], C[sa]);
+      }
+      if (c == kChC / 2 - 1 && H < L::Sets) {
+        // halfway: store the first half of the next chunk's fragments and
+        // load the second
+        if (ch + 1 < NC) {
+          #pragma unroll
+          for (int j = 0; j < H; ++j) {
+            const int f = wave + kChWaves * j;
+            if (f < kChC * R) ch_set_store<R>(st[j], f, stage(ch + 1));
+          }
+        }
+        #pragma unroll
+        for (int j = 0; j < H; ++j)
+          ch_set_load<R>(p, chn, min(wave + kChWaves * (H + j), kChC * R - 1), st[j]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (ch + 1 < NC) {
+      const int j0 = H < L::Sets ? H : 0;
+      #pragma unroll
+      for (int j = 0; j < H; ++j) {
+        const int f = wave + kChWaves * (j0 + j);
+        if (j0 + j < L::Sets && f < kChC * R) ch_set_store<R>(st[j], f, stage(ch + 1));
+      }
+      ch_scales_store<R>(ss, scales(ch + 1));
+    }
+    __syncthreads();
+  }
+}
+
+template <int R, bool DIAG>
+__global__ __launch_bounds__(kChWaves * 64) void skinny_chunk_kernel(GemmArgs p, int kp) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  using L = ChLayout<R>;
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int T = kp * kChC;
+  const int tb = T * wave / kChWaves, te = T * (wave + 1) / kChWaves;
+  const int q0 = tb / kChC;
+  const int pbase = blockIdx.x * kp;
+
+  f32x4 C[kChSeg][R];
+  #pragma unroll
+  for (int s = 0; s < kChSeg; ++s)
+    #pragma unroll
+    for (int r = 0; r < R; ++r) C[s][r] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // prologue: chunk 0 staged
+  {
+    ChSet st[L::Sets];
+    ChScales<R> ss;
+    #pragma unroll
+    for (int j = 0; j < L::Sets; ++j) ch_set_load<R>(p, 0, min(wave + kChWaves * j, kChC * R - 1), st[j]);
+    ch_scales_load<R>(p, 0, ss);
+    #pragma unroll
+    for (int j = 0; j < L::Sets; ++j) {
+      const int f = wave + kChWaves * j;
+      if (f < kChC * R) ch_set_store<R>(st[j], f, smem);
+    }
+    ch_scales_store<R>(ss, reinterpret_cast<float*>(smem + L::Stage));
+  }
+  __syncthreads();
+  switch (tb % kChC) {
+    case 0: ch_run<R, DIAG, 0>(p, smem, pbase, tb, te, C); break;
+    case 1: ch_run<R, DIAG, 1>(p, smem, pbase, tb, te, C); break;
+    case 2: ch_run<R, DIAG, 2>(p, smem, pbase, tb, te, C); break;
+    default: ch_run<R, DIAG, 3>(p, smem, pbase, tb, te, C); break;
+  }
+  if constexpr (DIAG) return;
+
+  // Store whole panels; a panel split between waves goes through LDS: the
+  // wave holding its first item adds the pieces of the following waves.
+  f32x4* part = reinterpret_cast<f32x4*>(smem);  // [waves][2][R][64]
+  #pragma unroll
+  for (int s = 0; s < kChSeg; ++s) {
+    const int q = q0 + s;
+    if (q * kChC >= te) continue;
+    const bool whole = q * kChC >= tb && (q + 1) * kChC <= te;
+    if (whole) {
+      const int col = 16 * (pbase + q) + r16;
+      #pragma unroll
+      for (int r = 0; r < R; ++r)
+        #pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int row = 16 * r + 4 * q4 + k;
+          if (row < p.M) p.out[(size_t)row * p.N + col] = __half_as_ushort(__float2half_rn(C[s][r][k]));
+        }
+    } else {
+      const int h = s == 0 ? 0 : 1;  // the range's first or last panel
+      #pragma unroll
+      for (int r = 0; r < R; ++r) part[((wave * 2 + h) * R + r) * 64 + lane] = C[s][r];
+    }
+  }
+  __syncthreads();
+  #pragma unroll
+  for (int s = 0; s < kChSeg; ++s) {
+    const int q = q0 + s;
+    if (q * kChC >= te) continue;
+    const bool whole = q * kChC >= tb && (q + 1) * kChC <= te;
+    if (whole || q * kChC < tb) continue;  // stored above, or started by an earlier wave
+    const int h = s == 0 ? 0 : 1;
+    f32x4 acc[R];
+    #pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = part[((wave * 2 + h) * R + r) * 64 + lane];
+    for (int v = wave + 1; v < kChWaves; ++v) {
+      const int vb = T * v / kChWaves, ve = T * (v + 1) / kChWaves;
+      if (vb >= (q + 1) * kChC) break;
+      if (ve > vb) {
+        #pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] += part[((v * 2 + 0) * R + r) * 64 + lane];
+      }
+    }
+    const int col = 16 * (pbase + q) + r16;
+    #pragma unroll
+    for (int r = 0; r < R; ++r)
+      #pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int row = 16 * r + 4 * q4 + k;
+        if (row < p.M) p.out[(size_t)row * p.N + col] = __half_as_ushort(__float2half_rn(acc[r][k]));
+      }
+  }
+}
+
+template <int R>
+const void* chunk_fn(bool diag) {
+  return diag ? reinterpret_cast<const void*>(&skinny_chunk_kernel<R, true>)
+              : reinterpret_cast<const void*>(&skinny_chunk_kernel<R, false>);
+}
+
+// Row blocks of the chunk kernel's instantiation for M rows.
+int chunk_r(int M) { return (M + 15) / 16; }
+
+const void* chunk_kernel(int R, bool diag) {
+  switch (R) {
+    case 1: return chunk_fn<1>(diag);
+    case 2: return chunk_fn<2>(diag);
+    case 3: return chunk_fn<3>(diag);
+    case 4: return chunk_fn<4>(diag);
+    default: return nullptr;
+  }
+}
+
+int chunk_lds(int R) {
+  switch (R) {
+    case 1: return ChLayout<1>::Bytes;
+    case 2: return ChLayout<2>::Bytes;
+    case 3: return ChLayout<3>::Bytes;
+    case 4: return ChLayout<4>::Bytes;
+    default: return 0;
+  }
+}
+
 }  // namespace
 
 bool skinny_stream_eligible(int M, int N, int K, int cus) {
   const int P = N / 16, NG = K / kG;
-  return M <= 8 && cus > 0 && P % cus == 0 && (P / cus) * NG >= kStreamWaves * 2 * kSB;
+  if (cus <= 0 || P % cus != 0) return false;
+  const int kp = P / cus;
+  if (M <= 8) return kp * NG >= kStreamWaves * 2 * kSB;
+  // 8 < M <= 64: every wave has at least three items (fewer leave the
+  // per-chunk staging and barrier unamortized) and at most kChItems
+  return M <= kChMaxM && kp * kChC >= 3 * kChWaves &&
+         (kp * kChC + kChWaves - 1) / kChWaves <= kChItems;
 }
 
 hipError_t set_skinny_attributes() {
@@ -877,10 +1289,24 @@ hipError_t set_skinny_attributes() {
     hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kStreamMaxLds);
     if (e != hipSuccess) return e;
   }
+  for (int R : {1, 2, 3, 4})
+    for (bool diag : {false, true}) {
+      hipError_t e = hipFuncSetAttribute(chunk_kernel(R, diag),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, chunk_lds(R));
+      if (e != hipSuccess) return e;
+    }
   return hipSuccess;
 }
 
 hipError_t launch_gemm_skinny(const GemmArgs& a, bool diag, hipStream_t stream) {
+  if (a.M > 8 && skinny_stream_eligible(a.M, a.N, a.K, a.cus)) {
+    const int R = chunk_r(a.M), kp = a.N / 16 / a.cus;
+    const void* fn = chunk_kernel(R, diag);
+    if (!fn) return hipErrorInvalidValue;
+    GemmArgs args = a;
+    void* params[] = {&args, const_cast<int*>(&kp)};
+    return hipLaunchKernel(fn, dim3(a.cus), dim3(kChWaves * 64), params, chunk_lds(R), stream);
+  }
   if (skinny_stream_eligible(a.M, a.N, a.K, a.cus)) {
     const int NG = a.K / kG, kp = a.N / 16 / a.cus;
     // the unpacked operand in LDS pays when it fits and a workgroup has

@@ -90,9 +90,11 @@ hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, b
 // and FMPQ quantization of h [M][I] with `map` into A / sa [I/G][M].
 hipError_t launch_swiglu_quantize(const uint16_t* GU, uint8_t* A, uint16_t* sa, int M, int I,
                                   const BlockMap& map, hipStream_t stream);
-// Few-token kernels (M <= kSkinnyMaxM): for M <= 8, when the 16-column
-// panels divide evenly over the CUs, a persistent kernel whose waves stream
-// contiguous runs of W_packed; otherwise one wave per (16 columns, split-K
+// Few-token kernels.  When the 16-column panels divide evenly over the CUs
+// (skinny_stream_eligible), persistent stream kernels whose workgroups own
+// whole panels: for M <= 8 the waves stream contiguous runs of W_packed; for
+// 8 < M <= 64 the K-blocks go in chunks whose activation fragments are staged
+// in LDS.  Otherwise (M <= kSkinnyMaxM) one wave per (16 columns, split-K
 // slot), or, for 8 < M <= 32 with at most two slots, four column blocks per
 // workgroup sharing the activation operand through LDS.
 constexpr int kSkinnyMaxM = 48;

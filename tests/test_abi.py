@@ -252,11 +252,18 @@ def test_stale_library_is_never_loaded(monkeypatch, tmp_path):
 
 def test_gemm_kernel_choice():
     k = comet.comet_gemm_kernel
-    # LLaMA-3-70B gate_up (N = 57344, 224 column tiles) on 256 CUs
-    assert [k(m, 57344, 8192, 256) for m in (1, 8, 16, 32, 33, 48, 64, 128, 129, 4096)] == \
-        [0, 0, 1, 1, 2, 2, 2, 2, 3, 3]
-    # narrow N keeps the few-token kernel up to 48 rows
-    assert [k(m, 8192, 8192, 256) for m in (33, 48, 49)] == [0, 0, 2]
+    # LLaMA-3-70B gate_up (N = 57344: 3584 panels, 14 per CU on 256 CUs): the
+    # stream kernels up to 64 rows, then 128-row and 256-row tiles
+    assert [k(m, 57344, 8192, 256) for m in (1, 8, 16, 32, 33, 48, 64, 65, 128, 129, 4096)] == \
+        [4, 4, 4, 4, 4, 4, 4, 2, 2, 3, 3]
+    # panels that do not divide over the CUs (304): few-token kernels up to 48
+    # rows (224 column tiles are too few for 304 CUs), 128-row tiles up to 128
+    assert [k(m, 57344, 8192, 304) for m in (1, 8, 16, 32, 33, 48, 64, 128, 129, 4096)] == \
+        [0, 0, 1, 1, 0, 0, 2, 2, 3, 3]
+    # one panel per CU: too few items for either stream kernel
+    assert [k(m, 4096, 8192, 256) for m in (8, 9, 33, 48, 49)] == [0, 0, 0, 0, 2]
+    # two panels per CU: the M <= 8 stream kernel only
+    assert [k(m, 8192, 8192, 256) for m in (8, 9, 33, 48, 49)] == [4, 1, 0, 0, 2]
     L = comet.lib()
     assert L.comet_gemm_kernel(16, 24, 256, 128, 256) == -1 and "N=24" in comet.comet_last_error()
     assert L.comet_gemm_kernel(16, 32, 256, 64, 256) == -1

@@ -108,10 +108,11 @@ def test_quantizer_edge_rows_through_gemm(M, N):
 
 @pytest.mark.parametrize("M", [33, 48])
 def test_wide_n_mid_rows_acc_window(M):
-    """LLaMA-3-70B gate_up at 33 and 48 rows runs on the 128-row tile kernel
-    (its 224 column tiles are wide): exact block sums over every row and a
-    column window across a tile boundary, and sampled fp16 rows."""
-    K, N = synth.LLAMA3_70B["gate_up"]
+    """33 and 48 rows at a gate_up-like width whose panels do not divide over
+    256 CUs (N = 57600: 225 column tiles, wide) run on the 128-row tile
+    kernel: exact block sums over every row and a column window across a
+    tile boundary, and sampled fp16 rows."""
+    K, N = 8192, 57600
     NG = K // 128
     assert comet.comet_gemm_kernel(M, N, K, 256) == 2
     prec = synth.prec_map(NG, NG // 16)
@@ -126,14 +127,17 @@ def test_wide_n_mid_rows_acc_window(M):
     assert_out_close(host_u16(r["out"]).view(np.float16)[rows], ref, f"wide-N M={M}")
 
 
-def test_fused_swiglu_wide_n_mid_rows():
-    """The fused SwiGLU entry point at M = 40 on the 70B gate_up shape (the
-    128-row kernel's fused epilogue) against the oracle's SwiGLU quantization
-    of the same GEMM's fp16 output."""
-    M, (K, N) = 40, synth.LLAMA3_70B["gate_up"]
+@pytest.mark.parametrize("N,kind", [(57344, "stream"), (57600, "mid")])
+def test_fused_swiglu_wide_n_mid_rows(N, kind):
+    """The fused SwiGLU entry point at M = 40, K = 8192: on the 70B gate_up
+    shape (stream kernel, then the standalone SwiGLU quantizer) and at N =
+    57600 (the 128-row kernel's fused epilogue), against the oracle's SwiGLU
+    quantization of the same GEMM's fp16 output."""
+    M, K = 40, 8192
     I = N // 2
     NG = K // 128
-    print(f"fused swiglu wide-N M={M}", flush=True)
+    assert comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, 256)] == kind
+    print(f"fused swiglu wide-N M={M} N={N} ({kind})", flush=True)
     prec = synth.prec_map(NG, NG // 16)
     A, sa = comet.quantize_act(dev_u16(synth.activations(40, M, K, prec)), prec)
     Wp, sw = comet.pack_w4(dev_u16(synth.weights(40, N, K)))
@@ -227,3 +231,37 @@ def test_quantizer_every_fp16_block_max():
     qa, osa = oracle.quantize_act(X16, prec)
     assert np.array_equal(host_u16(sa), osa)
     assert np.array_equal(host(A), oracle.pack_act(qa, prec))
+
+
+CHUNK = [
+    # (M, N, K, map kind): the chunked stream kernel (8 < M <= 64) runs when
+    # the 16-column panels divide evenly over the CUs (256 here) with at
+    # least three items per wave.  7 panels per workgroup: 3 or 4 items per
+    # wave, panels split between waves at every offset within a chunk
+    (9, 28672, 1152, "random"),       # one row block; last chunk partial (9 blocks)
+    (16, 28672, 512, "cfg0"),         # one chunk
+    (17, 28672, 1152, "alternate"),   # two row blocks, ragged rows
+    (40, 65536, 1664, "all8"),        # 16 panels per workgroup: eight items per wave
+    (64, 28672, 640, "random"),       # four row blocks
+    (33, 57344, 384, "cfg0"),         # 14 panels per workgroup (LLaMA-3-70B gate_up width)
+]
+
+
+@pytest.mark.parametrize("M,N,K,kind", CHUNK)
+def test_chunk_stream_kernel_matches_oracle(M, N, K, kind):
+    from test_gpu_parity import make_map
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    NG = K // 128
+    prec = make_map(kind, NG, seed=N + M)
+    print(f"chunk stream kernel M={M} N={N} K={K} {kind}", flush=True)
+    assert comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, cus)] == "stream"
+    win = (max(0, M - 40), M, N // 2 - 24, N // 2 + 40)
+    r = run_path(M, N, K, prec, seed=M + K, diag_window=win)
+    qa, sa = oracle.quantize_act(r["X16"], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    assert np.array_equal(host(r["acc"]), oracle.group_acc(qa[win[0]:win[1]], qw[win[2]:win[3]]))
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"chunk {M}x{N}x{K}")
+    again = comet.w4ax_gemm(r["A"], prec, r["sa"], r["Wp"], r["sw"], M, N, K)
+    assert torch.equal(r["out"].view(torch.int16), again.view(torch.int16))
