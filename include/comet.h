@@ -93,7 +93,7 @@ typedef enum {
   COMET_KERNEL_FEW_TOKEN_SHARED = 1,  /* the same, activations shared through LDS */
   COMET_KERNEL_MID = 2,               /* 128-row tiles */
   COMET_KERNEL_TILE = 3,              /* 256-row tiles */
-  COMET_KERNEL_STREAM = 4             /* up to 128 rows, weight panels divided evenly over the CUs */
+  COMET_KERNEL_STREAM = 4             /* up to 64 rows, weight panels divided evenly over the CUs */
 } comet_kernel_t;
 
 typedef enum {

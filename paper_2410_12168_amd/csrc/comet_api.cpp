@@ -176,7 +176,8 @@ std::string sched_mode() {
 // (and each wave gets enough of them).  Otherwise the few-token kernels take
 // M <= 48, except that above 32 rows the 128-row tile kernel takes over when
 // its 256-column tiles cover at least 3/4 of the CUs (wide N); the 128-row
-// tile kernel runs up to M = 128, the 256-row one above.
+// tile kernel runs up to M = 128; above, comet::choose_tile_m picks 128 or
+// 256 rows from the shape.
 int kernel_kind(int M, int N, int K, int cus) {
   if (comet::skinny_stream_eligible(M, N, K, cus)) return COMET_KERNEL_STREAM;
   const int col_tiles = (N + comet::kTileN - 1) / comet::kTileN;
@@ -185,13 +186,14 @@ int kernel_kind(int M, int N, int K, int cus) {
     return comet::skinny_shared(M, comet::skinny_splits(N, K, cus))
                ? COMET_KERNEL_FEW_TOKEN_SHARED
                : COMET_KERNEL_FEW_TOKEN;
-  return comet::gemm_tile_m(M) == comet::kTileMSmall ? COMET_KERNEL_MID : COMET_KERNEL_TILE;
+  return comet::choose_tile_m(M, N, K, comet::kG, cus) == comet::kTileMSmall ? COMET_KERNEL_MID
+                                                                             : COMET_KERNEL_TILE;
 }
 
-comet::PlanOptions plan_options(int M, int cus, const std::string& mode) {
+comet::PlanOptions plan_options(int M, int N, int K, int cus, const std::string& mode) {
   comet::PlanOptions opt;
   opt.num_cus = cus;
-  opt.tile_m = comet::gemm_tile_m(M);
+  opt.tile_m = comet::choose_tile_m(M, N, K, comet::kG, cus);
   opt.tile_n = comet::kTileN;
   opt.mode = mode;
   return opt;
@@ -242,7 +244,7 @@ comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* pr
   }
   DevicePlan dp;
   std::string err;
-  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, cus, mode), &dp.host, &err))
+  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, N, K, cus, mode), &dp.host, &err))
     return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
   const PlanBlob b = plan_blob(dp.host, prec);
   const std::vector<int>& blob = b.v;
@@ -493,13 +495,13 @@ comet_status_t run_gemm_noalloc(const uint8_t* A, const uint8_t* prec, const uin
   std::string mode = sched_mode();
   comet::Plan h;
   std::string err;
-  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, info.cus, mode), &h, &err))
+  if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, N, K, info.cus, mode), &h, &err))
     return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
   const size_t tile_bytes = (size_t)h.tile_m * h.tile_n * sizeof(float);
   if ((size_t)h.partial_slots * tile_bytes > comet::kNoallocPartialBytes ||
       (size_t)h.partial_slots * sizeof(int) > comet::kNoallocCounterBytes) {
     mode = "dp";
-    if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, info.cus, mode), &h, &err))
+    if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, N, K, info.cus, mode), &h, &err))
       return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
   }
   const PlanBlob b = plan_blob(h, prec);
@@ -770,7 +772,7 @@ comet_status_t comet_schedule_query(int M, int N, int K, int G, const uint8_t* p
   if (st) return st;
   comet::BlockMap map;
   if ((st = make_map(prec, K / G, &map))) return st;
-  comet::PlanOptions opt = plan_options(M, num_cus, sched_mode());
+  comet::PlanOptions opt = plan_options(M, N, K, num_cus, sched_mode());
   comet::Plan plan;
   std::string err;
   if (!comet::build_plan(M, N, K, G, prec, opt, &plan, &err))

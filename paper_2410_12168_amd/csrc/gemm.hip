@@ -617,33 +617,52 @@ __device__ __forceinline__ void store_tile(const GemmArgs& p, const WorkUnit& un
   const int r16 = lane & 15, q4 = lane >> 4;
   const int wr = (wave >> 2) * Geo<TM>::WM, wc = (wave & 3) * kWN;
   if (unit.nslots > 1) {
-    // split tile: publish this slot's partial, then the last arriver reduces
+    // Split tile.  Each slot publishes its fp32 partial and counts in;
+    // whichever counts in last adds the partials in slot order.  A tile of
+    // two slots needs only the other slot's partial: the plan puts the
+    // first slot early in its workgroup's list and the second at the end, so
+    // the second usually finds the first arrived and then skips publishing
+    // its own.  One device-scope release and one acquire per tile slot, by
+    // one thread: on this multi-XCD part each is a write-back or invalidate
+    // of the whole L2, too costly to issue from every wave.
     const int base = plan_at(p.split_index, unit.tile);
-    float* part = p.partials + (size_t)(base + unit.slot) * (TM * kTileN);
-    #pragma unroll
-    for (int rb = 0; rb < kRB; ++rb)
-      #pragma unroll
-      for (int cb = 0; cb < kCB; ++cb)
-        *reinterpret_cast<f32x4*>(part + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4) =
-            C[rb][cb];
-    // One device-scope release and one acquire per tile slot, by one
-    // thread: on this multi-XCD part each is a write-back or invalidate of
-    // the whole L2, too costly to issue from every wave.  The barrier first
-    // completes every wave's partial stores into L2.
-    __syncthreads();
+    const bool pair = unit.nslots == 2;
     if (threadIdx.x == 0) {
-      __threadfence();
-      const bool last = atomicAdd(p.counters + base, 1) == unit.nslots - 1;
-      if (last) __threadfence();
-      *s_last = last;
+      *s_last = pair && __hip_atomic_load(p.counters + base, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT) == 1;
+      if (*s_last) __threadfence();  // acquire the other slot's partial
     }
     __syncthreads();
-    if (!*s_last) return;
-    #pragma unroll
-    for (int rb = 0; rb < kRB; ++rb)
+    if (!*s_last) {
+      float* part = p.partials + (size_t)(base + unit.slot) * (TM * kTileN);
       #pragma unroll
-      for (int cb = 0; cb < kCB; ++cb) C[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < unit.nslots; ++s) {
+      for (int rb = 0; rb < kRB; ++rb)
+        #pragma unroll
+        for (int cb = 0; cb < kCB; ++cb)
+          *reinterpret_cast<f32x4*>(part + (((wave * kRB + rb) * kCB + cb) * 64 + lane) * 4) =
+              C[rb][cb];
+      // the barrier completes every wave's partial stores into L2
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        __threadfence();
+        const bool last = atomicAdd(p.counters + base, 1) == unit.nslots - 1;
+        if (last) __threadfence();
+        *s_last = last;
+      }
+      __syncthreads();
+      if (!*s_last) return;
+    }
+    // A pair adds the other slot's partial to its registers (two terms: the
+    // same sum whichever slot adds it); otherwise all partials in slot order.
+    const int s_first = pair ? unit.slot ^ 1 : 0;
+    const int s_end = pair ? s_first + 1 : unit.nslots;
+    if (!pair) {
+      #pragma unroll
+      for (int rb = 0; rb < kRB; ++rb)
+        #pragma unroll
+        for (int cb = 0; cb < kCB; ++cb) C[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int s = s_first; s < s_end; ++s) {
       const float* src = p.partials + (size_t)(base + s) * (TM * kTileN);
       #pragma unroll
       for (int rb = 0; rb < kRB; ++rb) {

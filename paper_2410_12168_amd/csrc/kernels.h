@@ -72,16 +72,14 @@ hipError_t launch_kv4_quantize(const uint16_t* X, uint8_t* codes, uint16_t* para
 hipError_t launch_kv4_dequantize(const uint8_t* codes, const uint16_t* params, uint16_t* out,
                                  int T, int C, int G, hipStream_t stream);
 
-// Output tile of one GEMM workgroup: kTileN columns and kTileM rows, or
-// kTileMSmall rows when M <= kTileMSmall (a taller tile would leave MFMA rows
-// idle).
+// Output tile of one GEMM workgroup: kTileN columns and kTileM or
+// kTileMSmall rows (comet::choose_tile_m decides from the shape).
 constexpr int kTileM = 256;
 constexpr int kTileMSmall = 128;
 constexpr int kTileN = 256;
-inline int gemm_tile_m(int M) { return M <= kTileMSmall ? kTileMSmall : kTileM; }
 
 // Persistent GEMM: `num_wgs` workgroups walk a.units (a.wg_begin per group);
-// tile_m is gemm_tile_m(a.M); swiglu selects the SwiGLU + quantize epilogue;
+// tile_m is the plan's tile height; swiglu selects the SwiGLU + quantize epilogue;
 // natural: the plan's K order is the map's own (not precision-batched), which
 // the SwiGLU epilogue does not support.
 hipError_t launch_gemm(const GemmArgs& a, int num_wgs, bool diag, bool swiglu, bool natural,

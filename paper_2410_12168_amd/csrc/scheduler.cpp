@@ -172,6 +172,19 @@ bool build_plan(int M, int N, int K, int G, const uint8_t* prec, const PlanOptio
     }
   }
 
+  // Within each workgroup: the split slots whose partial another slot will
+  // add first, whole tiles next, and the slots that finish a split tile
+  // last.  The early partials are then written while the chip still
+  // computes, and a finishing slot usually finds the others arrived, so it
+  // reads their partials and keeps its own in registers.
+  for (std::vector<PlanUnit>& v : per) {
+    auto rank = [](const PlanUnit& u) {
+      return u.nslots == 1 ? 1 : (u.slot < u.nslots - 1 ? 0 : 2);
+    };
+    std::stable_sort(v.begin(), v.end(),
+                     [&](const PlanUnit& a, const PlanUnit& b) { return rank(a) < rank(b); });
+  }
+
   // Flatten, and record the cost balance.
   p.wg_begin.push_back(0);
   double sum = 0;
@@ -188,6 +201,38 @@ bool build_plan(int M, int N, int K, int G, const uint8_t* prec, const PlanOptio
   p.mean_wg_cost = nw ? sum / nw : 0;
   *plan = std::move(p);
   return true;
+}
+
+// Tile height.  Up to 128 rows a 128-row tile (a taller one would leave MFMA
+// rows idle).  Above that, a 256-row tile does one K-block in about 2.1 us
+// on MI355X against about 1.35 us for a 128-row tile, so per row it is the
+// cheaper unit of work, but there are half as many tiles.  When that leaves a
+// fractional last wave that the plan splits (build_plan, "cost" mode), the
+// split costs a fixup of about 25 us: every split tile's fp32 partials are
+// written and read back at the end of the launch, all at once.  The estimate
+// below prices both heights that way (per workgroup: the K-blocks it runs,
+// plus the fixup if any tile is split, plus ~4 us more prologue and epilogue
+// for the smaller tile) and keeps 256 rows unless 128 is 3% faster: e.g.
+// 2048 x 4096 x 4096 on 256 CUs has 128 tiles of 256 rows, each split in
+// two, or 256 tiles of 128 rows, one per workgroup.
+int choose_tile_m(int M, int N, int K, int G, int cus) {
+  constexpr int kSmall = 128, kLarge = 256, kTileCols = 256;
+  if (M <= kSmall || cus <= 0 || G <= 0) return M <= kSmall ? kSmall : kLarge;
+  const PlanOptions defaults;
+  const long long NG = K / G, P = cus;
+  auto estimate = [&](int tm, double us_per_block, double extra_us) {
+    const long long T = (long long)((M + tm - 1) / tm) * ((N + kTileCols - 1) / kTileCols);
+    bool split = false;
+    long long blocks = (T + P - 1) / P * NG;
+    if (T % P != 0 && (double)(P - T % P) / P > defaults.split_min_idle) {
+      split = true;
+      blocks = (T * NG + P - 1) / P;
+    }
+    return blocks * us_per_block + (split ? 25.0 : 0.0) + extra_us;
+  };
+  const double t_large = estimate(kLarge, 2.1, 0.0);
+  const double t_small = estimate(kSmall, 1.35, 4.0);
+  return t_small < 0.97 * t_large ? kSmall : kLarge;
 }
 
 int skinny_splits(int N, int K, int cus) {

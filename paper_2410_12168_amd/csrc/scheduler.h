@@ -65,4 +65,9 @@ struct PlanOptions {
 bool build_plan(int M, int N, int K, int G, const uint8_t* prec, const PlanOptions& opt,
                 Plan* plan, std::string* err);
 
+// Output tile height (rows) for an M x N x K GEMM on `cus` workgroups of
+// 256-column tiles: 128 up to 128 rows, else 256 unless 128-row tiles are
+// estimated clearly faster (see scheduler.cpp).
+int choose_tile_m(int M, int N, int K, int G, int cus);
+
 }  // namespace comet

@@ -52,3 +52,20 @@ def test_down_half_8bit_random_placement():
     M, NG = 4096, K // 128
     check_sampled(M, N, K, synth.prec_map(NG, NG // 2, "random", seed=5), seed=13,
                   rows=np.array([1, 511, 2600, 4094]), what="70B down, half 8-bit random")
+
+
+def test_128_row_tiles_above_128_rows_ragged():
+    # M = 1900 rows, N = K = 4096 on 256 CUs: 240 tiles of 128 rows (the last
+    # row tile ragged, 108 rows) beat 128 split tiles of 256 rows, so the
+    # 128-row kernel runs with many row tiles; rows on both sides of every
+    # kind of boundary are checked
+    import torch
+    import paper_2410_12168_amd as comet
+    M, N, K = 1900, 4096, 4096
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if cus == 256:
+        assert comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, cus)] == "mid"
+    NG = K // 128
+    check_sampled(M, N, K, synth.prec_map(NG, 3, "random", seed=7), seed=14,
+                  rows=np.array([0, 127, 128, 1023, 1791, 1792, 1899]),
+                  what="128-row tiles, M = 1900")

@@ -94,6 +94,42 @@ def test_tile_height_follows_m():
         assert s["tile_m"] == want and s["tile_n"] == 256
 
 
+@pytest.mark.parametrize("M,N,K,want", [
+    (2048, 4096, 4096, 128),    # 128 tiles of 256 rows, all split; 256 of 128 rows: one each
+    (2048, 4096, 14336, 256),   # the same tiles, but a long K amortizes the split
+    (2048, 6144, 4096, 256),    # 192 tiles of 256 rows: a quarter idle, not split
+    (2048, 28672, 4096, 256),
+    (4096, 10240, 8192, 256),
+    (256, 57344, 8192, 256)])
+def test_tile_height_from_the_shape(M, N, K, want):
+    # above 128 rows the plan prices both heights (K-blocks per workgroup,
+    # plus the split fixup) and keeps 256 rows unless 128 is clearly faster
+    prec = np.full(K // 128, 4, np.uint8)
+    s = comet.comet_schedule_query(M, N, K, prec)
+    assert s["tile_m"] == want
+    kind = comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, 256)]
+    assert kind == ("mid" if want == 128 else "tile")
+    # the 128-row plan splits nothing here: one tile per workgroup
+    if want == 128:
+        units = s["units"]
+        assert (units[:, 4] == 1).all() and len(units) == 256
+
+
+@pytest.mark.parametrize("M,N,K", [(4096, 10240, 8192), (2048, 28672, 4096), (512, 8192, 8192),
+                                   (300, 1024, 1024)])
+def test_split_slots_ordered_within_workgroup(M, N, K):
+    # a workgroup runs the slots whose partial another slot adds first, whole
+    # tiles next and the slots that finish a split tile last
+    prec = synth.prec_map(K // 128, K // 128 // 16)
+    s = comet.comet_schedule_query(M, N, K, prec)
+    u, wgb = s["units"], s["wg_begin"]
+    rank = np.where(u[:, 4] == 1, 1, np.where(u[:, 3] < u[:, 4] - 1, 0, 2))
+    assert (rank != 1).any()
+    for w in range(s["num_wgs"]):
+        r = rank[wgb[w]:wgb[w + 1]]
+        assert (np.diff(r) >= 0).all(), (w, r)
+
+
 @pytest.mark.parametrize("M,N,split", [(128, 57344, False),   # 224 tiles: 12.5% of a wave idle
                                        (4096, 7936, False),   # 496 tiles: 6% idle
                                        (4096, 10240, True),   # 640 tiles: half a wave idle
