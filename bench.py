@@ -413,15 +413,31 @@ def _to_dev(a16, dev):
     return torch.from_numpy(np.ascontiguousarray(a16).view(np.int16)).to(dev).view(torch.float16)
 
 
-def _ms_per_call(fn, n: int, warm: int = 2) -> float:
-    """Average time of `fn(i)` over n back-to-back calls, from HIP events
-    around the batch on the current stream (the one the library launches on)."""
+def _ms_per_call(fn, n: int, warm: int = 2, min_ms: float = 20.0) -> float:
+    """Average time of `fn(i)` over back-to-back calls, from HIP events around
+    the batch on the current stream (the one the library launches on).
+
+    After the host-side setup between measurements the GPU has idled and its
+    clock ramps back up over the first milliseconds of work, so every
+    measurement first runs at least `min_ms` of untimed calls (and at least
+    `warm`), then times at least n calls and at least `min_ms` of them."""
+    import math
+
     import torch
 
     for i in range(warm):
         fn(i)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    fn(0)
+    e1.record()
+    torch.cuda.synchronize()
+    reps = max(1, math.ceil(min_ms / max(e0.elapsed_time(e1), 1e-3)))
+    for i in range(reps):
+        fn(i)
+    n = max(n, reps)
+    torch.cuda.synchronize()
     e0.record()
     for i in range(n):
         fn(i)
