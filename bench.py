@@ -69,11 +69,24 @@ def gemm_kind(M: int, N: int, K: int, cus: int) -> str:
     return comet.KERNEL_NAMES[comet.comet_gemm_kernel(M, N, K, cus)]
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and blank lines, so that a comment edit
+    does not mark a kernel as changed.  (The kernel sources hold no string
+    literal with a comment marker in it.)"""
+    import re
+
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = (re.sub(r"//.*", "", line).rstrip() for line in text.splitlines())
+    return "\n".join(line for line in lines if line.strip())
+
+
 def kernel_sha(kind: str) -> str:
+    """SHA-256 of the code (comments and blank lines removed) of the sources
+    that determine this kernel."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[kind]:
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(CSRC, name), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 
@@ -103,11 +116,39 @@ def profiled_traffic(kind: str, workload: str, layer: str, M: int):
         return None
 
 
+def warm_up(warmup, step) -> int:
+    """Run the untimed warm-up steps and return how many ran: `warmup` if
+    given, else 5 and then, for short steps, as many more as cover 20 ms of
+    GPU work (one of them timed with events to size the rest), because the
+    clock ramps up over the first milliseconds of work."""
+    import math
+
+    import torch
+
+    n = 5 if warmup is None else warmup
+    for _ in range(n):
+        step()
+    if warmup is not None:
+        return n
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    step()
+    e1.record()
+    torch.cuda.synchronize()
+    extra = max(0, math.ceil(20.0 / max(e0.elapsed_time(e1), 1e-3)) - n - 1)
+    for _ in range(extra):
+        step()
+    return n + 1 + extra
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default: 5, or more for short steps: enough "
+                         "for 20 ms of GPU work, since the clock ramps up over the first "
+                         "milliseconds)")
     ap.add_argument("--workload", default="llama3-70b-prefill", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--m", type=int, default=0, help="tokens (default: the workload's)")
@@ -216,29 +257,26 @@ def main():
             if ev is not None:
                 ev[i][2].record()
 
-    for _ in range(args.warmup):
-        step()
+    args.warmup = warm_up(args.warmup, step)
     torch.cuda.synchronize()
 
-    # timed region: whole steps
+    # timed region: whole steps; then, queued right behind it so that the GPU
+    # does not idle in between, the same steps again with events around each
+    # launch (same stream) for the per-kernel durations
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     start.record()
     for _ in range(args.steps):
         step()
     stop.record()
-    torch.cuda.synchronize()
-    ms_total = start.elapsed_time(stop)
-    ms_per_step = ms_total / args.steps
-
-    # per-kernel launch durations (events around each launch, same stream)
-    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
-           for _ in range(args.steps)]
-    torch.cuda.synchronize()
     for s in range(args.steps):
         step(evs[s])
     torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_per_step = ms_total / args.steps
     q_ms = np.zeros(len(layers))
     g_ms = np.zeros(len(layers))
     for s in range(args.steps):
@@ -686,8 +724,7 @@ def bench_mlp(args, wl, dev):
             ev[1].record()
         comet.comet_w4ax_gemm(A2, prec2, sa2, Wp2, sw2, y, M, N2, K2)
 
-    for _ in range(args.warmup):
-        step()
+    args.warmup = warm_up(args.warmup, step)
     torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
@@ -754,8 +791,7 @@ def bench_kv4(args, wl, dev):
             if ev is not None:
                 ev[i][1].record()
 
-    for _ in range(args.warmup):
-        step()
+    args.warmup = warm_up(args.warmup, step)
     torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)

@@ -56,8 +56,9 @@ constexpr int kCB = kWN / 16;
 constexpr int kWr = kTileN * 64;          // one packed weight K-block, ring of three
 static_assert(kTileN == 4 * kWN, "8 waves as 2 x 4 quadrants");
 
-// Geometry of a tile of TM rows (TM = 256, or 128 for 64 < M <= 128, where a
-// 256-row tile would leave half of every MFMA idle): 8 waves as 2 x 4
+// Geometry of a tile of TM rows (TM = 256, or 128: for 64 < M <= 128, where a
+// 256-row tile would leave half of every MFMA idle, and for larger M where
+// comet::choose_tile_m finds 128-row tiles faster): 8 waves as 2 x 4
 // quadrants of (TM / 2) x 64.
 template <int TM>
 struct Geo {
@@ -775,9 +776,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 
 
 // ---------------------------------------------------------------------------
-// Mid-size GEMM (up to 128 rows; see kernel_kind for where it runs): 128-row
-// tiles, with the workgroup's waves
-// split by role so that no load is waited for early.  With this few rows the
+// Mid-size GEMM: 128-row tiles (up to 128 rows, and above where
+// comet::choose_tile_m finds them faster), with the workgroup's waves split
+// by role so that no load is waited for early.  With this few rows the
 // weights come from HBM exactly once and a K-block computes briefly, so the
 // loads need several K-blocks of lead, and a wait on the vector-memory counter
 // covers every older load of the wave:
