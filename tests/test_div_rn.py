@@ -5,7 +5,7 @@ binary32 neighbour of it (the hardware reciprocal is within one ulp of 1/s);
 the scale itself, RN(amax / qmax), is computed the same way with r = RN(1/qmax).  Because
 s is a binary16 value (at most 11 significant bits) this q equals RN(x / s)
 for every binary32 x (Markstein's correction step; the margin argument is in
-csrc/quantize.hip).  These tests check the identity on the CPU:
+csrc/fmpq.h).  These tests check the identity on the CPU:
 exhaustively over all binary16 operand pairs the activation and weight
 quantizers can see, and over every binary16 scale with random and
 near-midpoint numerators for the KV4 quantizer."""
