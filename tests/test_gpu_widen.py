@@ -29,15 +29,20 @@ def tile_rows(M, tile=256, seed=0):
 
 
 @pytest.mark.parametrize("model,layer", [("70b", "qkv"), ("70b", "o"), ("70b", "gate_up"),
-                                         ("70b", "down"), ("8b", "gate_up"), ("8b", "down")])
+                                         ("70b", "down"), ("8b", "qkv"), ("8b", "o"),
+                                         ("8b", "gate_up"), ("8b", "down")])
 def test_one_row_per_row_tile_full_size(model, layer):
+    # one row in every row tile of the height the schedule picks (the 8B o
+    # layer runs 128-row tiles, the others 256)
     shapes, M = (synth.LLAMA3_70B, 4096) if model == "70b" else (synth.LLAMA3_8B, 2048)
     K, N = shapes[layer]
     NG = K // 128
-    print(f"row tiles {model} {layer} M={M} N={N} K={K}", flush=True)
     prec = synth.prec_map(NG, NG // 16)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    tm = comet.comet_schedule_query(M, N, K, prec, num_cus=cus)["tile_m"]
+    print(f"row tiles {model} {layer} M={M} N={N} K={K} tile_m={tm}", flush=True)
     r = run_path(M, N, K, prec, seed=21)
-    rows = tile_rows(M, seed=NG)
+    rows = tile_rows(M, tile=tm, seed=NG)
     qa, sa = oracle.quantize_act(r["X16"][rows], prec)
     assert np.array_equal(act_rows(host(r["A"]), prec, M, rows), oracle.pack_act(qa, prec))
     qw, sw = oracle.quantize_weight(r["W16"])
@@ -70,6 +75,30 @@ def test_split_tile_acc_window_production_plan():
     ref = oracle.dequant_gemm(qa, sa, qw, sw)
     out = host_u16(r["out"]).view(np.float16)[win[0]:win[1], win[2]:win[3]]
     assert_out_close(out, ref, "split tile window")
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 8192, 8192), (2048, 4096, 14336)])
+def test_split_tiles_sum_in_slot_order(M, N, K):
+    """Plans whose tiles are split: 512 x 8192 x 8192 cuts each of its 64
+    tiles into four slots (all partials added in slot order); the 8B down
+    projection's 128 tiles into two (the finishing slot adds the other's
+    partial to its registers).  The fp16 output must match the oracle and be
+    bit-identical from run to run, whichever slot arrives last."""
+    NG = K // 128
+    prec = synth.prec_map(NG, NG // 16, "random", seed=M)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    q = comet.comet_schedule_query(M, N, K, prec, num_cus=cus)
+    nslots = q["units"][:, 4].max()
+    print(f"split slots M={M} N={N} K={K}: up to {nslots} slots per tile", flush=True)
+    assert nslots >= 2
+    r = run_path(M, N, K, prec, seed=41)
+    rows = tile_rows(M, tile=q["tile_m"], seed=3)
+    qa, sa = oracle.quantize_act(r["X16"][rows], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16)[rows], ref, f"split {M}x{N}x{K}")
+    again = comet.w4ax_gemm(r["A"], prec, r["sa"], r["Wp"], r["sw"], M, N, K)
+    assert torch.equal(r["out"].view(torch.int16), again.view(torch.int16))
 
 
 @pytest.mark.parametrize("M,N", [(6, 64), (6, 512), (70, 256), (300, 512)])
