@@ -210,6 +210,21 @@ def test_llama3_70b_decode_full_size(M):
     assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"decode M={M}")
 
 
+@pytest.mark.parametrize("layer,M", [("qkv", 1), ("qkv", 8), ("o", 1), ("o", 8), ("down", 1),
+                                     ("down", 8)])
+def test_llama3_70b_decode_other_layers_full_size(layer, M):
+    # the other LLaMA-3-70B layers at decode sizes (per-wave few-token kernel
+    # for qkv's 640 panels, the stream kernel for o and down with two panels
+    # per CU): every output row checked
+    K, N = synth.LLAMA3_70B[layer]
+    prec = synth.prec_map(K // 128, K // 128 // 16)
+    r = run_path(M, N, K, prec, seed=M + 7)
+    qa, sa = oracle.quantize_act(r["X16"], prec)
+    qw, sw = oracle.quantize_weight(r["W16"])
+    ref = oracle.dequant_gemm(qa, sa, qw, sw)
+    assert_out_close(host_u16(r["out"]).view(np.float16), ref, f"decode {layer} M={M}")
+
+
 @pytest.mark.parametrize("M", [40, 96, 128])
 def test_llama3_70b_decode_128_row_tiles_sampled_rows(M):
     # LLaMA-3-70B gate_up with 128-row tiles (at M = 40 too: its 224 column
