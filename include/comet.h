@@ -58,7 +58,8 @@
  *   - The 128- and 256-row tile kernels run from a schedule (plan) that the
  *     library builds on the host and uploads on the first call for each
  *     (device, M, N, K, map, mode): that call allocates a few KB of device
- *     memory and waits for the upload.  Plans stay cached until
+ *     memory and enqueues the upload on its stream, ahead of the kernel (the
+ *     host does not wait for it).  Plans stay cached until
  *     comet_release_caches(), so the cache grows with every distinct shape;
  *     the few-token kernels (small M) need no plan.
  *   - The environment variable COMET_SCHED selects the schedule mode (Sec.

@@ -146,6 +146,7 @@ struct PlanKey {
 
 struct DevicePlan {
   comet::Plan host;
+  std::vector<int> blob;  // the uploaded array, kept: the copy is asynchronous
   void* dmem = nullptr;  // units | wg_begin | order | split_index, one allocation
   const comet::WorkUnit* units = nullptr;
   const int* wg_begin = nullptr;
@@ -246,14 +247,15 @@ comet_status_t get_plan(int dev, int cus, int M, int N, int K, const uint8_t* pr
   std::string err;
   if (!comet::build_plan(M, N, K, comet::kG, prec, plan_options(M, N, K, cus, mode), &dp.host, &err))
     return fail(COMET_ERR_INVALID_ARG, "%s", err.c_str());
-  const PlanBlob b = plan_blob(dp.host, prec);
-  const std::vector<int>& blob = b.v;
+  PlanBlob b = plan_blob(dp.host, prec);
+  dp.blob = std::move(b.v);
   if (std::getenv("COMET_TEST_FAIL_ALLOC")) return fail(COMET_ERR_OOM, "plan allocation failed (forced)");
-  hipError_t e = hipMalloc(&dp.dmem, blob.size() * sizeof(int));
+  hipError_t e = hipMalloc(&dp.dmem, dp.blob.size() * sizeof(int));
   if (e != hipSuccess) return fail(COMET_ERR_OOM, "plan allocation: %s", hipGetErrorString(e));
-  e = hipMemcpyAsync(dp.dmem, blob.data(), blob.size() * sizeof(int), hipMemcpyHostToDevice,
-                     stream);
-  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  // enqueued on the call's stream ahead of the kernel that reads it; the
+  // host array lives in the cache entry, so nobody waits for the copy
+  e = hipMemcpyAsync(dp.dmem, dp.blob.data(), dp.blob.size() * sizeof(int),
+                     hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) {
     (void)hipFree(dp.dmem);
     return fail(COMET_ERR_HIP, "plan upload: %s", hipGetErrorString(e));
