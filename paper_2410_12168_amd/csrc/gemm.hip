@@ -710,12 +710,45 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
   __syncthreads();
   const uint32_t wvoff = w_lane_off();
 
-  for (int u = plan_at(p.wg_begin, blockIdx.x); u < u_end; ++u) {
-    const int* ue = reinterpret_cast<const int*>(p.units) + 5 * u;
-    const WorkUnit unit{plan_at(ue, 0), plan_at(ue, 1), plan_at(ue, 2), plan_at(ue, 3),
-                        plan_at(ue, 4)};
-    const int tm = unit.tile / p.tiles_n, tn = unit.tile % p.tiles_n;
-    const int m0 = tm * TM, n0 = tn * kTileN;
+  const bool awave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4;
+  // The unit whose first K-block loads are in flight: they are issued before
+  // the previous unit's epilogue, so their latency overlaps its stores.
+  WorkUnit unit{};
+  int m0 = 0, n0 = 0;
+  KBlock k0{};
+  WPanels wp{};
+  StageScales sc{};
+  auto issue = [&](int uu) {
+    const int* ue = reinterpret_cast<const int*>(p.units) + 5 * uu;
+    unit = WorkUnit{plan_at(ue, 0), plan_at(ue, 1), plan_at(ue, 2), plan_at(ue, 3),
+                    plan_at(ue, 4)};
+    m0 = (unit.tile / p.tiles_n) * TM;
+    n0 = (unit.tile % p.tiles_n) * kTileN;
+    k0 = kblock(order_at(p, unit.g_begin));
+    wp = w_panels(p, n0);
+    if (awave) {
+      act_dma(p, k0, m0, lds + 2 * kBuf + 3 * kWr, lds);
+      sc = scales_load(p, k0.g, m0, n0);
+    } else {
+      dma_w(wp, wvoff, k0.g, lds + 2 * kBuf);
+      if (unit.g_begin + 1 < unit.g_end)
+        dma_w(wp, wvoff, kblock(order_at(p, unit.g_begin + 1)).g, lds + 2 * kBuf + kWr);
+    }
+  };
+  int u = plan_at(p.wg_begin, blockIdx.x);
+  if (u < u_end) issue(u);
+  for (; u < u_end; ++u) {
+    // the unit's first K-block in place (and its second's weights in flight)
+    if (awave) {
+      wait_vm_all();
+      if (!k0.b8) act_unpack(smem + 2 * kBuf + 3 * kWr, smem);
+      scales_store<TM>(sc, smem);
+    } else if (unit.g_begin + 1 < unit.g_end) {
+      asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    } else {
+      wait_vm_all();
+    }
+    barrier_lds();
 
     f32x4 C[kRB][kCB];
     #pragma unroll
@@ -725,24 +758,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 
     // software pipeline over the unit's K-blocks; the schedule lists all
     // 4-bit blocks before the 8-bit ones, so each precision runs its own loop
-    const KBlock k0 = kblock(order_at(p, unit.g_begin));
-    const WPanels wp = w_panels(p, n0);
-    if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4) {
-      act_dma(p, k0, m0, lds + 2 * kBuf + 3 * kWr, lds);
-      const StageScales sc = scales_load(p, k0.g, m0, n0);
-      wait_vm_all();
-      if (!k0.b8) act_unpack(smem + 2 * kBuf + 3 * kWr, smem);
-      scales_store<TM>(sc, smem);
-    } else {
-      dma_w(wp, wvoff, k0.g, lds + 2 * kBuf);
-      if (unit.g_begin + 1 < unit.g_end) {
-        dma_w(wp, wvoff, kblock(order_at(p, unit.g_begin + 1)).g, lds + 2 * kBuf + kWr);
-        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-      } else {
-        wait_vm_all();
-      }
-    }
-    barrier_lds();
     if constexpr (NAT) {
       // natural order: one K-loop per run of equal precision, the loads
       // running on across runs
@@ -768,9 +783,12 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
         kloop<TM, DIAG, true>(p, o, smem, lds, s_order, unit.g_begin, split, unit.g_end,
                               unit.g_end, NG, m0, n0, wp, wvoff, C);
     }
+    const WorkUnit cur = unit;
+    const int cm0 = m0, cn0 = n0;
+    if (u + 1 < u_end) issue(u + 1);  // LDS is free: the K-loop ended on a barrier
     if (DIAG) continue;
 
-    store_tile<TM, SWIGLU>(p, unit, m0, n0, C, &s_last, smem);
+    store_tile<TM, SWIGLU>(p, cur, cm0, cn0, C, &s_last, smem);
   }
 }
 
