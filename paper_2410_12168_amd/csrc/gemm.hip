@@ -6,7 +6,8 @@
 // becomes two such FP8 bytes, hi = m >> 3 (0..15) and lo = m & 7, so that
 // code = 8 * hi + lo.  Each 16x16 output block of one K-block is one
 // v_mfma_f32_16x16x128_f8f6f4 (K = 128 = one block) for W4A4 and two for
-// W4A8.  Products of such codes are integers times 2^-18 and their sums stay
+// W4A8, the second (hi) chained on the first's result with an E8M0 block
+// scale of 2^3 on A.  Products of such codes are integers times 2^-18 and their sums stay
 // below 2^24 units, so the fp32 MFMA result is the exact block sum (the
 // paper's integer tile result, Sec. 4.1) and needs no int->float convert.
 // Dequantization (Sec. 4.3: the scale absorbs the conversion factor) runs on
@@ -415,17 +416,12 @@ __device__ __forceinline__ void compute_block(const uint8_t* buf, const uint8_t*
       }
     }
     f32x4 y = mfma_fp8(af, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
-    f32x4 yh;
-    if constexpr (B8) yh = mfma_fp8(ah, wf[cb], f32x4{0.f, 0.f, 0.f, 0.f});
+    if constexpr (B8) y = mfma_fp8_x8(ah, wf[cb], y);  // + 8 * hi, exact
     hook(s);
     if (cb == kCB - 1 && rb + 1 < kRB) {
       // the next row block's fragment replaces this one in the same registers
       __builtin_amdgcn_sched_barrier(0);
       af = lds_frag(buf + o.fa0 + (rb + 1) * 2048, buf + o.fa1 + (rb + 1) * 2048);
-    }
-    if constexpr (B8) {
-      #pragma unroll
-      for (int i = 0; i < 4; ++i) y[i] = __builtin_fmaf(yh[i], 8.0f, y[i]);  // exact
     }
     if constexpr (DIAG) {
       const int col = n0 + wc + cb * 16 + r16;

@@ -162,8 +162,8 @@ __device__ __forceinline__ void compute_step(const GemmArgs& p, const u32x4& wra
         ah[k] = (int)hi8(s.a[r][0][k]);
         ah[4 + k] = (int)hi8(x1[k]);
       }
-      const f32x4 yh = mfma_fp8(ah, wf, f32x4{0.f, 0.f, 0.f, 0.f});
-      y = mfma_fp8(al, wf, yh * 8.0f);  // exact: integers below 2^24 units
+      // exact: integers below 2^24 units
+      y = mfma_fp8_x8(ah, wf, mfma_fp8(al, wf, f32x4{0.f, 0.f, 0.f, 0.f}));
     } else {
       u32x4 alo, ahi;
       unpack4(s.a[r][0], alo, ahi);
@@ -404,8 +404,8 @@ __device__ __forceinline__ void compute_shared(const GemmArgs& p, const u32x4& w
         ah[k] = (int)hi8(x0[k]);
         ah[4 + k] = (int)hi8(x1[k]);
       }
-      const f32x4 yh = mfma_fp8(ah, wf, f32x4{0.f, 0.f, 0.f, 0.f});
-      y = mfma_fp8(al, wf, yh * 8.0f);  // exact: integers below 2^24 units
+      // exact: integers below 2^24 units
+      y = mfma_fp8_x8(ah, wf, mfma_fp8(al, wf, f32x4{0.f, 0.f, 0.f, 0.f}));
     } else {
       const i32x8 af = {(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3],
                         (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};
@@ -662,8 +662,8 @@ __device__ __forceinline__ void stream_step(const GemmArgs& p, const uint8_t* sA
       const u32x4 l1 = *reinterpret_cast<const u32x4*>(fa + 1040);
       const i32x8 al = {(int)l0[0], (int)l0[1], (int)l0[2], (int)l0[3],
                         (int)l1[0], (int)l1[1], (int)l1[2], (int)l1[3]};
-      const f32x4 yh = mfma_fp8(af, wf, f32x4{0.f, 0.f, 0.f, 0.f});
-      y = mfma_fp8(al, wf, yh * 8.0f);  // exact: integers below 2^24 units
+      // exact: integers below 2^24 units
+      y = mfma_fp8_x8(af, wf, mfma_fp8(al, wf, f32x4{0.f, 0.f, 0.f, 0.f}));
     } else {
       y = mfma_fp8(af, wf, f32x4{0.f, 0.f, 0.f, 0.f});
     }
@@ -681,8 +681,7 @@ __device__ __forceinline__ void stream_step(const GemmArgs& p, const uint8_t* sA
         ah[k] = (int)hi8(xa[k]);
         ah[4 + k] = (int)hi8(x1[k]);
       }
-      const f32x4 yh = mfma_fp8(ah, wf, f32x4{0.f, 0.f, 0.f, 0.f});
-      y = mfma_fp8(al, wf, yh * 8.0f);
+      y = mfma_fp8_x8(ah, wf, mfma_fp8(al, wf, f32x4{0.f, 0.f, 0.f, 0.f}));
     } else {
       u32x4 alo, ahi;
       unpack4(xa, alo, ahi);
@@ -1030,8 +1029,8 @@ __device__ __forceinline__ void ch_group(const GemmArgs& p, const ChW& xa, const
         ah[4 + k] = (int)hi8(x1[k]);
       }
       // exact: integers below 2^24 units
-      ya = mfma_fp8(al, wa, mfma_fp8(ah, wa, f32x4{0.f, 0.f, 0.f, 0.f}) * 8.0f);
-      if constexpr (TWO) yb = mfma_fp8(al, wb, mfma_fp8(ah, wb, f32x4{0.f, 0.f, 0.f, 0.f}) * 8.0f);
+      ya = mfma_fp8_x8(ah, wa, mfma_fp8(al, wa, f32x4{0.f, 0.f, 0.f, 0.f}));
+      if constexpr (TWO) yb = mfma_fp8_x8(ah, wb, mfma_fp8(al, wb, f32x4{0.f, 0.f, 0.f, 0.f}));
     } else {
       const i32x8 af = {(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3],
                         (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};

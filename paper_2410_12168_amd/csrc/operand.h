@@ -4,7 +4,9 @@
 // that (w & 0x87878787) and (rotr(w, 4) & 0x87878787) are OCP FP8-E4M3
 // subnormal bytes equal to code * 2^-9 (codes 0..3 and 4..7 of the dword).
 // An 8-bit byte (sign, 7-bit magnitude m) splits into two such bytes,
-// hi = m >> 3 (0..15) and lo = m & 7, with code = 8 * hi + lo.
+// hi = m >> 3 (0..15) and lo = m & 7, with code = 8 * hi + lo (a 4-bit hi is
+// exact too: with its top bit in the exponent field the byte is the first
+// normal binade, (8 + (hi & 7)) * 2^-9).
 // v_mfma_f32_16x16x128_f8f6f4 multiplies these exactly: products are integers
 // times 2^-18 and a K-block's sum stays below 2^24 units, so the fp32 result
 // is the exact integer block sum scaled by 2^-18.
@@ -39,6 +41,15 @@ __device__ __forceinline__ f32x4 mfma_fp8(const i32x8& a, const i32x8& b, f32x4 
   // cbsz = blgp = 0: both operands OCP FP8-E4M3; zero scale operands select
   // the unscaled instruction.
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// The same with A's products scaled by 2^3 through the instruction's E8M0
+// block scales (130 for A on every lane, 127 = 2^0 for B): chained after the
+// low part's MFMA it adds 8 * hi * w for the high parts of 8-bit codes into
+// the same accumulator, exactly, with no vector instruction.
+__device__ __forceinline__ f32x4 mfma_fp8_x8(const i32x8& a, const i32x8& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, (int)0x82828282u, 0,
+                                                          0x7F7F7F7F);
 }
 
 __device__ __forceinline__ f32x4 scale_products(float sa, float sw) {
