@@ -47,7 +47,7 @@ struct PlanOptions {
   int tile_m = 128;
   int tile_n = 128;
   double cost4 = 1.0;   // relative cost of a 4-bit K-block of one tile
-  double cost8 = 1.6;   // relative cost of an 8-bit K-block of one tile
+  double cost8 = 1.7;   // relative cost of an 8-bit K-block of one tile
   // "cost" mode splits the last wave of tiles only if leaving it unsplit
   // would idle more than this share of the workgroups
   double split_min_idle = 0.3;

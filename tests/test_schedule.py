@@ -11,7 +11,7 @@ import pytest
 import paper_2410_12168_amd as comet
 import synth
 
-COST4, COST8 = 1.0, 1.6
+COST4, COST8 = 1.0, 1.7
 
 
 def check_plan(M, N, K, prec, num_cus=256):
