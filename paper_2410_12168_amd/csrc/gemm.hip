@@ -796,13 +796,16 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 // weights come from HBM exactly once and a K-block computes briefly, so the
 // loads need several K-blocks of lead, and a wait on the vector-memory counter
 // covers every older load of the wave:
-//   * waves 0-3 only issue direct loads: a K-block's packed weights and its
-//     fp16 weight scales, into a ring of four slots three K-blocks ahead, and
-//     wait for them with counted waits;
-//   * waves 4-7 stage the activation codes and scales (few rows, written just
+//   * waves 0-3 stage the activation codes and scales (few rows, written just
 //     before by the quantizer, so they come from L2) through registers one
 //     K-block ahead, unpack 4-bit codes once and store them to a
-//     double-buffered LDS stage;
+//     double-buffered LDS stage.  They win issue arbitration over the waves
+//     sharing their SIMDs, so this extra work runs while waves 4-7 still
+//     compute (as in the tile kernel; with the roles the other way round the
+//     kernel ran 4-6% slower);
+//   * waves 4-7 only issue direct loads: a K-block's packed weights and its
+//     fp16 weight scales, into a ring of four slots three K-blocks ahead, and
+//     wait for them with counted waits;
 //   * all eight waves compute their 64 x 64 quadrant with the tile kernel's
 //     K-block step.
 // As in the tile kernel, both roles issue their loads a few MFMA steps into
@@ -816,20 +819,20 @@ constexpr int kMidLds = 2 * kMidStage + kMidD * kMidSlot;
 static_assert(kMidTM * 136 * 2 <= kMidLds, "SwiGLU epilogue buffer fits in the mid kernel's LDS");
 constexpr int kMidVm = 5;  // direct loads per K-block and weight wave
 
-// Waves 0-3: packed weights of K-block g (16 KB, four 1 KB loads per wave, in
-// the ring layout of dma_w) and the fp16 scales of the slot's 256 columns
-// (lanes 0-7 of each wave: columns n0 + 64 wave + 8 lane .. + 7, at byte
+// Waves 4-7 (w = wave - 4): packed weights of K-block g (16 KB, four 1 KB
+// loads per wave, in the ring layout of dma_w) and the fp16 scales of the
+// slot's 256 columns (lanes 0-7 of each wave: columns n0 + 64 w + 8 lane .. + 7, at byte
 // kWr + 2 * (column - n0)).  Columns past N re-read the last valid ones.
 __device__ __forceinline__ void mid_dma(const GemmArgs& p, int g, int n0, uint32_t slot) {
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3;
   #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int j = 4 * wave + i;
+    const int j = 4 * w + i;
     dma16nt(w_src(p, g, n0, j), slot + j * 1024);
   }
-  const int c0 = min(n0 + 64 * wave + 8 * (lane & 7), p.N - 8);
-  if (lane < 8) dma16(p.sw + (size_t)g * p.N + c0, slot + kWr + 128 * wave);
+  const int c0 = min(n0 + 64 * w + 8 * (lane & 7), p.N - 8);
+  if (lane < 8) dma16(p.sw + (size_t)g * p.N + c0, slot + kWr + 128 * w);
 }
 
 // Wait until at most n of this wave's direct loads are in flight (n = 0, 5
@@ -852,11 +855,11 @@ __device__ __forceinline__ f32x4 slot_sw(const uint8_t* slot) {
                __half2float(__ushort_as_half(sw[32])), __half2float(__ushort_as_half(sw[48]))};
 }
 
-// Waves 4-7 (t = threadIdx.x - 256): one K-block's activation codes and scale.
+// Waves 0-3 (t = threadIdx.x): one K-block's activation codes and scale.
 // 4-bit block: chunk t % 4 of rows t / 4 + 64 i (i < 2); 8-bit block: chunk
 // t % 8 of rows t / 8 + 32 i (i < 4).  Rows past M are clamped.
 __device__ __forceinline__ void mid_load(const GemmArgs& p, const KBlock& kb, int m0, Stage& st) {
-  const int t = threadIdx.x - 256;
+  const int t = threadIdx.x;
   const uint8_t* A = p.A + (size_t)p.M * 64 * (size_t)kb.aoff;
   const uint32_t b8 = kb.b8 ? 1u : 0u;
   #pragma unroll
@@ -877,7 +880,7 @@ __device__ __forceinline__ void mid_load(const GemmArgs& p, const KBlock& kb, in
 }
 
 __device__ __forceinline__ void mid_store(const Stage& st, bool b8, uint8_t* buf) {
-  const int t = threadIdx.x - 256;
+  const int t = threadIdx.x;
   if (!b8) {
     const int r = t >> 2, c = t & 3;
     #pragma unroll
@@ -905,7 +908,7 @@ __device__ __forceinline__ void mid_loop(const GemmArgs& p, const LaneOffsets& o
                                          uint32_t lds, const int* order, int pos, int end, int gb,
                                          int ge, int NG, int m0, int n0, Stage& st,
                                          f32x4 (&C)[Geo<kMidTM>::RB][kCB]) {
-  const bool wwave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4;
+  const bool wwave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) >= 4;
   for (; pos < end; ++pos) {
     const int j = pos - gb;
     const KBlock kb = kblock(__builtin_amdgcn_readfirstlane(order[pos]));
@@ -937,7 +940,7 @@ __global__ __launch_bounds__(kThreads) void gemm_mid_kernel(GemmArgs p) {
   const int NG = p.K / kG;
   const LaneOffsets o = lane_offsets<TM>();
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
-  const bool wwave = threadIdx.x < 256;
+  const bool wwave = threadIdx.x >= 256;
   const int u_end = plan_at(p.wg_begin, blockIdx.x + 1);
   for (int i = threadIdx.x; i < NG; i += kThreads) s_order[i] = p.order[i];
   __syncthreads();
