@@ -802,7 +802,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs p) {
 //     double-buffered LDS stage.  They win issue arbitration over the waves
 //     sharing their SIMDs, so this extra work runs while waves 4-7 still
 //     compute (as in the tile kernel; with the roles the other way round the
-//     kernel ran 4-6% slower);
+//     kernel ran 2-6% slower);
 //   * waves 4-7 only issue direct loads: a K-block's packed weights and its
 //     fp16 weight scales, into a ring of four slots three K-blocks ahead, and
 //     wait for them with counted waits;
