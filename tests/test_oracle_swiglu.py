@@ -72,6 +72,34 @@ def test_swiglu_f16_against_fp64():
         assert abs(exact[i] - mid) <= 8 * ulp32(exact[i]) + 1e-12
 
 
+def test_swiglu_f16_every_gate_value():
+    """Every finite fp16 gate value with a few up values: the oracle's fp16 h is
+    within one fp16 ulp of fp16 of the fp64 SwiGLU, and equal to it except where
+    the fp64 value lies within fp32 rounding of an fp16 rounding boundary."""
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    gv_all = bits.view(np.float16)
+    g = bits[np.isfinite(gv_all)]
+    gv = g.view(np.float16).astype(np.float64)
+    for upv in (1.0, -0.75, 3.0517578125e-05, 1000.0):
+        u = np.full(g.shape, np.float16(upv)).view(np.uint16)
+        with np.errstate(over="ignore", invalid="ignore"):
+            exact = gv / (1.0 + np.exp(-gv)) * np.float64(np.float16(upv))
+            ref = exact.astype(np.float16)
+        h = oracle.swiglu_f16(g, u).view(np.float16)
+        fin = np.isfinite(ref)
+        # beyond the fp16 range both overflow to the same infinity
+        assert np.array_equal(np.isinf(h[~fin]), np.isinf(ref[~fin]))
+        hf, rf, ef = h[fin].astype(np.float64), ref[fin].astype(np.float64), exact[fin]
+        with np.errstate(over="ignore"):  # above 65504 the next fp16 value is inf
+            sp = np.spacing(np.abs(ref[fin])).astype(np.float64)
+        assert np.all(np.abs(hf - rf) <= sp), upv
+        diff = np.flatnonzero(hf != rf)
+        assert diff.size <= 0.01 * hf.size, (upv, diff.size)
+        for i in diff:
+            mid = (hf[i] + rf[i]) / 2
+            assert abs(ef[i] - mid) <= 8 * ulp32(ef[i]) + 1e-12, (upv, gv[fin][i])
+
+
 @pytest.mark.parametrize("M,I,G", [(3, 256, 128), (5, 64, 16), (1, 128, 128)])
 def test_swiglu_quantize_grouping(M, I, G):
     NG = I // G
