@@ -7,9 +7,10 @@
 // code = 8 * hi + lo.  Each 16x16 output block of one K-block is one
 // v_mfma_f32_16x16x128_f8f6f4 (K = 128 = one block) for W4A4 and two for
 // W4A8, the second (hi) chained on the first's result with an E8M0 block
-// scale of 2^3 on A.  Products of such codes are integers times 2^-18 and their sums stay
-// below 2^24 units, so the fp32 MFMA result is the exact block sum (the
-// paper's integer tile result, Sec. 4.1) and needs no int->float convert.
+// scale of 2^3 on A.  Products of such codes are integers times 2^-18 and
+// their sums stay below 2^24 units, so the fp32 MFMA result is the exact
+// block sum (the paper's integer tile result, Sec. 4.1) and needs no
+// int->float convert.
 // Dequantization (Sec. 4.3: the scale absorbs the conversion factor) runs on
 // the vector ALUs, once per output and K-block:
 //     C += Y * P,   P = (sa * 2^18) * sw      (fp32; sa * sw is exact),
@@ -821,8 +822,9 @@ constexpr int kMidVm = 5;  // direct loads per K-block and weight wave
 
 // Waves 4-7 (w = wave - 4): packed weights of K-block g (16 KB, four 1 KB
 // loads per wave, in the ring layout of dma_w) and the fp16 scales of the
-// slot's 256 columns (lanes 0-7 of each wave: columns n0 + 64 w + 8 lane .. + 7, at byte
-// kWr + 2 * (column - n0)).  Columns past N re-read the last valid ones.
+// slot's 256 columns (lanes 0-7 of each wave: columns n0 + 64 w + 8 lane
+// .. + 7, at byte kWr + 2 * (column - n0)).  Columns past N re-read the last
+// valid ones.
 __device__ __forceinline__ void mid_dma(const GemmArgs& p, int g, int n0, uint32_t slot) {
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3;
