@@ -4,10 +4,10 @@ Each case quantizes, packs and multiplies through the C ABI and checks the
 per-block int32 sums of a window bit-exactly and the whole fp16 output
 against the oracle's tolerance.  The shapes are drawn once from a fixed
 seed, spread over the few-token (M <= 8), shared-activation (8 < M <= 32),
-three-row-block few-token (32 < M <= 48), mid-size (48 < M <= 128) and
-tile (M > 128) kernels, with ragged M, N and K, small column counts that
-make the tile kernel split every tile over many workgroups, and all four
-precision-map kinds.  The oracle's cost bounds the sizes.
+three-row-block few-token (32 < M <= 48), 128-row (48 < M <= 128) and
+256-row tile (M > 128, up to several row tiles) kernels, with ragged M, N
+and K, small column counts that make the tile kernels split every tile over
+many workgroups, and all the precision-map kinds.  The oracle's cost bounds the sizes.
 """
 import numpy as np
 import pytest
@@ -18,11 +18,11 @@ from test_gpu_parity import host, host_u16, make_map, run_path
 
 pytestmark = pytest.mark.gpu
 
-REGIMES = [(1, 8), (9, 32), (33, 48), (49, 128), (129, 400)]
+REGIMES = [(1, 8), (9, 32), (33, 48), (49, 128), (129, 400), (401, 1100)]
 KINDS = ["cfg0", "all4", "all8", "alternate", "random"]
 
 
-def sweep_shapes(n_per_regime=5, seed=20241016, budget=2.5e8):
+def sweep_shapes(n_per_regime=6, seed=20241016, budget=2.5e8):
     rng = np.random.default_rng(seed)
     shapes = []
     for lo, hi in REGIMES:
