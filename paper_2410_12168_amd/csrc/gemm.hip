@@ -508,8 +508,8 @@ __device__ __forceinline__ void kloop(const GemmArgs& p, const LaneOffsets& o, u
       if (!inside) act_dma(p, kn, m0, lds + kRaw, lds + (cur ^ 1) * kBuf);
     }
     auto hook = [&](int s) {
-      if (s == 2 && !awave && wnext) dma_w(wp, wvoff, g2, wdst);
-      if (s == 3 && awave && more && inside) {
+      if (s == 1 && !awave && wnext) dma_w(wp, wvoff, g2, wdst);
+      if (s == 2 && awave && more && inside) {
         if (!kn.b8) {
           #pragma unroll
           for (int i = 0; i < 4; ++i) act_dma4_in(Anext, m0, i, al, lds + kRaw);
