@@ -18,7 +18,7 @@ from test_gpu_parity import host, host_u16, make_map, run_path
 
 pytestmark = pytest.mark.gpu
 
-REGIMES = [(1, 8), (9, 32), (33, 48), (49, 128), (129, 400), (401, 1100)]
+REGIMES = [(1, 8), (9, 32), (33, 48), (49, 128), (129, 400), (401, 1100), (1101, 2100)]
 KINDS = ["cfg0", "all4", "all8", "alternate", "random"]
 
 
