@@ -1018,7 +1018,7 @@ __device__ __forceinline__ void ch_group(const GemmArgs& p, const ChW& xa, const
       n0v = *reinterpret_cast<const u32x4*>(fr + (r + 1) * ChLayout<R>::Frag);
       n1v = *reinterpret_cast<const u32x4*>(fr + (r + 1) * ChLayout<R>::Frag + 16);
     }
-    f32x4 ya, yb;
+    f32x4 ya, yb = {0.f, 0.f, 0.f, 0.f};  // yb: second panel (TWO) only
     if (b8) {
       i32x8 al, ah;
       #pragma unroll
