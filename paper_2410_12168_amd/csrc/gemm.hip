@@ -83,10 +83,13 @@ struct Geo {
 // c ^ (r & 7) swizzle runs at 60% of the read bandwidth).
 __device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ ((r ^ (r >> 1)) & 7)) << 4); }
 
-// Packed weights in a ring slot: column c's 64 bytes (one K-block) at c * 64,
-// its 16-byte chunk j (32 codes) at slot j ^ ((c >> 2) & 3), so that the 16
-// columns read by each 16-lane phase of a ds_read_b128 hit distinct banks.
-__device__ __forceinline__ int wswz(int c, int j) { return c * 64 + ((j ^ ((c >> 2) & 3)) << 4); }
+// Packed weights in a ring slot: one kilobyte per 16-column panel (one
+// K-block of it), chunk-major inside: tile column c's 16-byte chunk j (32
+// codes) at (c / 16) * 1024 + (16 j + c % 16) * 16.  A fragment read (lane
+// r16 + 16 q4 takes chunk q4 of column r16 of a panel) is then one linear
+// kilobyte, free of bank conflicts on gfx950 (measured: a column-major panel
+// with swizzled chunks read at 60% of the LDS bandwidth).
+__device__ __forceinline__ int wpos(int c, int j) { return (c >> 4) * 1024 + ((j << 4) + (c & 15)) * 16; }
 
 // Scales of one stage (floats after the A codes): the activation scale of
 // tile row r at r, so a lane's four rows 4 j .. 4 j + 3 of a row block are one
@@ -108,8 +111,9 @@ __device__ __forceinline__ i32x8 lds_frag(const uint8_t* p0, const uint8_t* p1) 
 }
 
 // Per-lane LDS offsets, fixed for the whole kernel.  Fragment reads of row
-// block rb (column block cb) add rb*2048 (cb*2048): 16 rows of 128 bytes, and
-// the swizzle term depends only on the row's low 4 bits, which do not change.
+// block rb add rb*2048 (16 rows of 128 bytes; the swizzle term depends only on
+// the row's low 4 bits, which do not change), of column block cb cb*1024 (one
+// weight panel).
 struct LaneOffsets {
   int fa0, fa1;   // A fragment chunks (2*q4, 2*q4+1) of row wr + r16
   int fw;         // packed weight chunk q4 of column wc + r16 (in a ring slot)
@@ -123,7 +127,7 @@ __device__ __forceinline__ LaneOffsets lane_offsets() {
   LaneOffsets o;
   o.fa0 = swz(wr + r16, 2 * q4);
   o.fa1 = swz(wr + r16, 2 * q4 + 1);
-  o.fw = wswz(wc + r16, q4);
+  o.fw = wpos(wc + r16, q4);
   (void)tid;
   return o;
 }
@@ -185,15 +189,14 @@ __device__ __forceinline__ void dma16nt(const void* g, uint32_t lds) {
 
 // Source of one 1 KB wave load of packed weights: K-block g of the 16-column
 // panel j of the tile at n0 (one contiguous kilobyte of W_packed).  Lane L
-// fills column 16 j + L / 4, slot L % 4 of the ring layout with the chunk
-// that wswz() places there.  Panels past N are clamped (their outputs are
-// never stored).
+// fills the ring layout's position L * 16 of the panel: chunk L / 16 of the
+// panel's column L % 16.  Panels past N are clamped (their outputs are never
+// stored).
 __device__ __forceinline__ const uint8_t* w_src(const GemmArgs& p, int g, int n0, int j) {
   const int lane = threadIdx.x & 63;
   const int NG = p.K / kG;
   const int panel = min(n0 / 16 + j, p.N / 16 - 1);
-  const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
-  return p.W + ((size_t)panel * NG + g) * 1024 + (lane >> 2) * 64 + chunk * 16;
+  return p.W + ((size_t)panel * NG + g) * 1024 + (lane & 15) * 64 + (lane >> 4) * 16;
 }
 
 // Direct load with a scalar base and a 32-bit per-lane byte offset.
@@ -204,8 +207,8 @@ __device__ __forceinline__ void dma16s(const uint8_t* base, uint32_t voff, uint3
 
 // Weight loads of waves 4-7: wave 4 + w loads panels 4 w .. 4 w + 3 of the
 // tile (clamped to the last panel past N).  Per tile, the panels' bases;
-// per lane, the offset of its column and chunk slot within a 1 KB K-block
-// (the ring layout of wswz()).
+// per lane, the source offset of its ring position within a 1 KB K-block
+// (the ring layout of wpos(): column lane % 16, chunk lane / 16).
 struct WPanels {
   const uint8_t* b[4];
 };
@@ -220,7 +223,7 @@ __device__ __forceinline__ WPanels w_panels(const GemmArgs& p, int n0) {
 }
 __device__ __forceinline__ uint32_t w_lane_off() {
   const int lane = threadIdx.x & 63;
-  return (lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) << 4);
+  return (lane & 15) * 64 + (lane >> 4) * 16;
 }
 
 // Packed weights of K-block g for the tile's 256 columns into a ring slot:
@@ -821,7 +824,7 @@ static_assert(kMidTM * 136 * 2 <= kMidLds, "SwiGLU epilogue buffer fits in the m
 constexpr int kMidVm = 5;  // direct loads per K-block and weight wave
 
 // Waves 4-7 (w = wave - 4): packed weights of K-block g (16 KB, four 1 KB
-// loads per wave, in the ring layout of dma_w) and the fp16 scales of the
+// loads per wave, in the ring layout of wpos()) and the fp16 scales of the
 // slot's 256 columns (lanes 0-7 of each wave: columns n0 + 64 w + 8 lane
 // .. + 7, at byte kWr + 2 * (column - n0)).  Columns past N re-read the last
 // valid ones.
