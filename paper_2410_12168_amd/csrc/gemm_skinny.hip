@@ -327,8 +327,10 @@ hipError_t launch_r(const GemmArgs& a, bool diag, hipStream_t stream) {
 // pipeline more than the weight stream once M reaches 8.  Here the four waves
 // of a slot load one batch of four K-blocks together, one K-block each,
 // unpack 4-bit codes once, and leave every MFMA fragment in a double-buffered
-// LDS area at [batch buffer][slot][K-block][row block][lane] (32 bytes each);
-// one barrier per batch publishes it.  Weights, scales and dequantization are
+// LDS area at [batch buffer][slot][K-block][row block] (2 KB each: all lanes'
+// first 16 bytes, then all lanes' second 16 bytes, so that both fragment
+// reads are linear and free of bank conflicts; 32 bytes per lane in a row
+// read at ~60% of the rate); one barrier per batch publishes it.  Weights, scales and dequantization are
 // those of the per-wave kernel.
 constexpr int kCBW = 4;  // column blocks per workgroup
 
@@ -370,8 +372,8 @@ __device__ __forceinline__ void chunk_store(const AChunk<R>& c, uint8_t* dst) {
   for (int r = 0; r < R; ++r) {
     u32x4 lo = c.v[r][0], hi = c.v[r][1];
     if (!c.b8) unpack4(c.v[r][0], lo, hi);
-    *reinterpret_cast<u32x4*>(dst + r * 2048 + lane * 32) = lo;
-    *reinterpret_cast<u32x4*>(dst + r * 2048 + lane * 32 + 16) = hi;
+    *reinterpret_cast<u32x4*>(dst + r * 2048 + lane * 16) = lo;
+    *reinterpret_cast<u32x4*>(dst + r * 2048 + 1024 + lane * 16) = hi;
   }
 }
 
@@ -392,8 +394,8 @@ __device__ __forceinline__ void compute_shared(const GemmArgs& p, const u32x4& w
                     (int)whi[0], (int)whi[1], (int)whi[2], (int)whi[3]};
   #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const u32x4 x0 = *reinterpret_cast<const u32x4*>(frag + r * 2048 + lane * 32);
-    const u32x4 x1 = *reinterpret_cast<const u32x4*>(frag + r * 2048 + lane * 32 + 16);
+    const u32x4 x0 = *reinterpret_cast<const u32x4*>(frag + r * 2048 + lane * 16);
+    const u32x4 x1 = *reinterpret_cast<const u32x4*>(frag + r * 2048 + 1024 + lane * 16);
     f32x4 y;
     if (b8) {
       i32x8 al, ah;
@@ -652,14 +654,17 @@ __device__ __forceinline__ void stream_step(const GemmArgs& p, const uint8_t* sA
                     (int)whi[0], (int)whi[1], (int)whi[2], (int)whi[3]};
   f32x4 y;
   if constexpr (LDSA) {
-    const uint8_t* fa = sA + (size_t)aoff * 1024 + (r16 & 7) * 128 + q4 * 32;
+    // row r16 & 7's chunks 2 q4 and 2 q4 + 1, at their swizzled positions
+    const int r8 = r16 & 7;
+    const uint8_t* fa = sA + (size_t)aoff * 1024 + r8 * 128 + (((2 * q4) ^ r8) << 4);
+    const uint8_t* fb = sA + (size_t)aoff * 1024 + r8 * 128 + (((2 * q4 + 1) ^ r8) << 4);
     const u32x4 a0 = *reinterpret_cast<const u32x4*>(fa);
-    const u32x4 a1 = *reinterpret_cast<const u32x4*>(fa + 16);
+    const u32x4 a1 = *reinterpret_cast<const u32x4*>(fb);
     const i32x8 af = {(int)a0[0], (int)a0[1], (int)a0[2], (int)a0[3],
                       (int)a1[0], (int)a1[1], (int)a1[2], (int)a1[3]};
     if (b8) {
       const u32x4 l0 = *reinterpret_cast<const u32x4*>(fa + 1024);
-      const u32x4 l1 = *reinterpret_cast<const u32x4*>(fa + 1040);
+      const u32x4 l1 = *reinterpret_cast<const u32x4*>(fb + 1024);
       const i32x8 al = {(int)l0[0], (int)l0[1], (int)l0[2], (int)l0[3],
                         (int)l1[0], (int)l1[1], (int)l1[2], (int)l1[3]};
       // exact: integers below 2^24 units
@@ -752,7 +757,9 @@ __global__ __launch_bounds__(kStreamWaves * 64) void skinny_stream_kernel(GemmAr
   // per workgroup: activation scales, block table (four entries past the end
   // wrap to blocks 0..3), and with LDSA the unpacked activation operand: for
   // every block and row r < 8 (clamped to M - 1) 128 FP8 bytes at aoff KB +
-  // 128 r, an 8-bit block's lo parts one KB after its hi parts
+  // 128 r, 16-byte chunk c at chunk position c ^ r (the eight rows a fragment
+  // read touches then sit on distinct banks; unswizzled, the read ran at ~58%
+  // of the rate), an 8-bit block's lo parts one KB after its hi parts
   for (int e = threadIdx.x; e < NG * 8; e += NW * 64)
     sSa[e] = p.sa[(size_t)(e >> 3) * p.M + min(e & 7, p.M - 1)];
   for (int e = threadIdx.x; e < NG + kSB; e += NW * 64) {
@@ -764,7 +771,7 @@ __global__ __launch_bounds__(kStreamWaves * 64) void skinny_stream_kernel(GemmAr
       const int gi = e >> 6, r = (e >> 3) & 7, c = e & 7;  // block, row, 16-code chunk
       const int ao = aoff_of(p, gi);
       const int row = min(r, p.M - 1);
-      uint8_t* dst = sA + (size_t)ao * 1024 + r * 128 + c * 16;
+      uint8_t* dst = sA + (size_t)ao * 1024 + r * 128 + ((c ^ r) << 4);
       if (!is8(p, gi)) {
         const uint2 v =
             *reinterpret_cast<const uint2*>(p.A + (size_t)ao * p.M * 64 + row * 64 + c * 8);
@@ -892,7 +899,7 @@ constexpr int kChMaxM = 64;               // rows (four row blocks)
 
 template <int R>
 struct ChLayout {
-  static constexpr int Frag = 2048;                   // one (K-block, row block): 64 lanes x 32 B
+  static constexpr int Frag = 2048;                   // one (K-block, row block): 2 x 64 lanes x 16 B
   static constexpr int Stage = kChC * R * Frag;       // a chunk's activation fragments
   static constexpr int Scales = kChC * 16 * R * 4;    // its fp32 activation scales (x 2^18)
   static constexpr int Buf = Stage + Scales;
@@ -930,9 +937,9 @@ __device__ __forceinline__ void ch_set_store(const ChSet& s, int f, uint8_t* sta
   const int lane = threadIdx.x & 63;
   u32x4 lo = s.v[0], hi = s.v[1];
   if (!s.b8) unpack4(s.v[0], lo, hi);
-  uint8_t* dst = stage + f * ChLayout<R>::Frag + lane * 32;  // f = c * R + r
+  uint8_t* dst = stage + f * ChLayout<R>::Frag + lane * 16;  // f = c * R + r
   *reinterpret_cast<u32x4*>(dst) = lo;
-  *reinterpret_cast<u32x4*>(dst + 16) = hi;
+  *reinterpret_cast<u32x4*>(dst + 1024) = hi;
 }
 
 // Activation scales of chunk ch: entry c * 16 R + row, fp16 loaded here,
@@ -1009,14 +1016,14 @@ __device__ __forceinline__ void ch_group(const GemmArgs& p, const ChW& xa, const
   const float swa = __half2float(__ushort_as_half((unsigned short)xa.sw));
   const float swb = __half2float(__ushort_as_half((unsigned short)xb.sw));
   // row block r + 1's fragment is read while row block r computes
-  const uint8_t* fr = sA + c * R * ChLayout<R>::Frag + lane * 32;
-  u32x4 n0v = *reinterpret_cast<const u32x4*>(fr), n1v = *reinterpret_cast<const u32x4*>(fr + 16);
+  const uint8_t* fr = sA + c * R * ChLayout<R>::Frag + lane * 16;
+  u32x4 n0v = *reinterpret_cast<const u32x4*>(fr), n1v = *reinterpret_cast<const u32x4*>(fr + 1024);
   #pragma unroll
   for (int r = 0; r < R; ++r) {
     const u32x4 x0 = n0v, x1 = n1v;
     if (r + 1 < R) {
       n0v = *reinterpret_cast<const u32x4*>(fr + (r + 1) * ChLayout<R>::Frag);
-      n1v = *reinterpret_cast<const u32x4*>(fr + (r + 1) * ChLayout<R>::Frag + 16);
+      n1v = *reinterpret_cast<const u32x4*>(fr + (r + 1) * ChLayout<R>::Frag + 1024);
     }
     f32x4 ya, yb = {0.f, 0.f, 0.f, 0.f};  // yb: second panel (TWO) only
     if (b8) {
