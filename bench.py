@@ -42,8 +42,10 @@ WORKLOADS = {
     "llama3-8b-prefill": dict(M=2048, layers="LLAMA3_8B"),
     # few-token regime: the gate_up layer streams its 4-bit weights from HBM
     "llama3-70b-decode": dict(M=8, layers="LLAMA3_70B", only="gate_up", rotate=6),
-    # LLaMA-3-70B MLP: quantize x, gate/up GEMM with SwiGLU and the down
-    # projection's quantization fused into its epilogue, down GEMM
+    # LLaMA-3-70B MLP: quantize x, the gate/up GEMM through the SwiGLU entry
+    # point (the down projection's input quantized in the GEMM epilogue on
+    # 128-row tiles, by the standalone SwiGLU kernel on the other paths),
+    # down GEMM
     "llama3-70b-mlp": dict(M=4096, mlp=True),
     # KV4 cache quantization of a prefill batch (8 prompts x 4096 tokens): the
     # K and V rows of every layer (8 KV heads x head_dim 128 = 1024 channels,
